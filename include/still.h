@@ -1,0 +1,162 @@
+/*
+ * still.h - C ABI of the MI355X (gfx950) Still compactor forward pass.
+ *
+ * Still (arxiv 2606.07878) compacts one transformer layer's KV cache
+ * (K, V in R^{H x N x d} per layer, keys RoPE-rotated by the base model) into
+ * t << N synthetic entries (C_k, C_v in R^{H x t x d}) with a small per-layer
+ * Perceiver (Section 2; Appendix A):
+ *   1. RoPE-fix: keys are inverse-rotated into a position-free frame
+ *      (Section 2.2; Appendix B, single-pass recipe step 3);
+ *   2. X^(h) = [K^(h); V^(h)] in R^{N x 2d} (Appendix A, input concatenation);
+ *   3. B pre-norm blocks on the latent bank Z in R^{H x t x d_l}:
+ *        Z'   = Z   + CrossAttn(RMSNorm(Z), X)
+ *        Z''  = Z'  + SelfAttn(RMSNorm(Z'))
+ *        Z''' = Z'' + FFN(RMSNorm(Z''))            (Appendix A, blocks)
+ *      cross-attention has n_c heads of width d_l each (expanded convention),
+ *      biased Q/K projections, L2 QK-norm, the compactor's own RoPE (latent
+ *      positions evenly spaced over [min p, max p]) and logits scaled by d_l;
+ *   4. C_k = Z_out W_key, C_v = Z_out W_val (Appendix A, output projections);
+ *   5. optional re-rotation of C_k at the latent (output) positions
+ *      (Appendix B, single-pass recipe step 5).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All tensor arguments are DEVICE pointers (memory allocated by the caller
+ *   on the current HIP device), except the arrays of per-layer pointers of
+ *   still_compact_model and the `blocks` array of still_layer_weights, which
+ *   are HOST arrays holding device pointers.  The library never allocates or
+ *   frees memory and keeps no device state between calls.
+ * - Row-major, densely packed layouts.  Matrices are stored [out][in]
+ *   (torch.nn.Linear layout): the paper's x W with W in R^{in x out} is
+ *   evaluated as x W^T with the stored [out][in] array.
+ * - Element type: STILL_MODE_BF16 -> every K, V, weight, bias, latent and
+ *   output buffer holds bfloat16; STILL_MODE_FP32 -> float32 (validation
+ *   mode, all internal arithmetic in fp32).  Positions are always float64.
+ * - Work is enqueued on `stream` (NULL = default stream) and the call returns
+ *   without synchronising.  Arguments are validated before anything is
+ *   enqueued; a non-OK status means nothing was launched.  Faults during
+ *   execution surface at the caller's next synchronisation.
+ * - Outputs must not alias inputs or the workspace.  NaN/Inf in the inputs
+ *   are not checked and propagate.
+ * - Calls that share a workspace must be ordered on one stream.
+ */
+#ifndef STILL_H_
+#define STILL_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  STILL_OK = 0,
+  STILL_E_INVAL = -1,        /* NULL pointer, bad enum, non-positive size       */
+  STILL_E_SHAPE = -2,        /* inconsistent shapes (e.g. t != latent bank size) */
+  STILL_E_DTYPE = -3,        /* unknown mode                                     */
+  STILL_E_WORKSPACE = -4,    /* workspace NULL or smaller than still_workspace_size */
+  STILL_E_UNSUPPORTED = -5,  /* valid per the paper but not supported by these kernels */
+  STILL_E_HIP = -6           /* a HIP runtime call failed (see still_last_error) */
+} still_status;
+
+typedef enum { STILL_MODE_BF16 = 0, STILL_MODE_FP32 = 1 } still_mode;
+typedef enum { STILL_FFN_NONE = 0, STILL_FFN_SWIGLU = 1, STILL_FFN_GELU = 2 } still_ffn;
+
+/* flags for the compaction calls */
+enum { STILL_F_REROTATE = 1 };   /* re-rotate C_k at the output positions */
+
+/* Hyper-parameters of one layer's compactor (Appendix A; canonical summary). */
+typedef struct {
+  int32_t n_kv_heads;        /* H, KV heads of the base model                         */
+  int32_t head_dim;          /* d, base-model KV head width (even)                    */
+  int32_t latent_dim;        /* D = d_l                                               */
+  int32_t n_blocks;          /* B >= 1                                                */
+  int32_t cross_every_block; /* 1: cross-attention in every block; 0: block 0 only    */
+  int32_t n_cross_heads;     /* n_c >= 1                                              */
+  int32_t cross_head_dim;    /* cross head width; 0 -> D (the paper's convention)     */
+  int32_t n_self_heads;      /* n_s; 0 disables latent self-attention                 */
+  int32_t self_head_dim;     /* self head width; 0 -> D                               */
+  int32_t ffn_kind;          /* still_ffn                                             */
+  int32_t ffn_hidden;        /* F, hidden width of the FFN                            */
+  int32_t final_norm;        /* 1: RMSNorm before the output heads                    */
+  float logit_scale_cross;   /* 0 -> cross head width (the d_l scale)                 */
+  float logit_scale_self;    /* 0 -> self head width                                  */
+  double compactor_rope_base;/* base of the compactor's internal RoPE (canonical 10)  */
+  float rms_eps;             /* RMSNorm epsilon (1e-6)                                */
+  float l2_eps;              /* QK-norm epsilon: x / max(||x||, l2_eps) (1e-12)       */
+  int32_t mode;              /* still_mode                                            */
+} still_config;
+
+/* One block's parameters (device pointers; [out][in] matrices).  Tensors of
+ * disabled sublayers are ignored and may be NULL.  A NULL bias means zero.
+ *   E_c = n_c * cross_head_dim,  E_s = n_s * self_head_dim,  F = ffn_hidden
+ *   ca_wq [E_c][D]  ca_bq [E_c]  ca_wk [E_c][2d]  ca_bk [E_c]
+ *   ca_wv [E_c][2d] ca_wo [D][E_c]
+ *   sa_wq [E_s][D]  sa_bq [E_s]  sa_wk [E_s][D]  sa_bk [E_s]
+ *   sa_wv [E_s][D]  sa_wo [D][E_s]
+ *   ffn_wg [F][D] ffn_wu [F][D] ffn_wd [D][F]   (GELU uses ffn_wu, ffn_wd) */
+typedef struct {
+  const void *ca_wq, *ca_bq, *ca_wk, *ca_bk, *ca_wv, *ca_wo;
+  const void *sa_wq, *sa_bq, *sa_wk, *sa_bk, *sa_wv, *sa_wo;
+  const void *ffn_wg, *ffn_wu, *ffn_wd;
+} still_block_weights;
+
+/* One layer's compactor: latent bank [H][t_bank][D], `blocks` is a HOST array
+ * of n_blocks entries, output heads w_key, w_val [d][D]. */
+typedef struct {
+  const void *latents;
+  int32_t t_bank;
+  const still_block_weights *blocks;
+  const void *w_key;
+  const void *w_val;
+} still_layer_weights;
+
+/* Bytes of device workspace needed by a call compacting N tokens to t with
+ * n_layers layers (the workspace is reused layer after layer).  Returns 0 if
+ * the configuration is invalid or unsupported. */
+size_t still_workspace_size(const still_config *cfg, int64_t N, int32_t t, int32_t n_layers);
+
+/* Compact one layer.
+ *   K, V        [H][N][d]  RoPE'd keys and values (device)
+ *   positions   [N]        float64 logical cache positions (device); any real
+ *                          values, not necessarily sorted or integral
+ *   rope_theta             base of the base model's RoPE (un-rotation and
+ *                          re-rotation use frequency theta^(-2j/d))
+ *   t                      compact length; must equal w->t_bank
+ *   flags                  STILL_F_REROTATE or 0
+ *   C_k, C_v    [H][t][d]  outputs (device, caller-allocated)
+ *   out_positions [t]      float64 output positions (device) or NULL:
+ *                          p_min + i (p_max - p_min)/(t-1)  (p_min if t == 1)
+ *   workspace              device buffer of >= still_workspace_size(cfg,N,t,1) bytes
+ *   stream                 hipStream_t (NULL = default stream)           */
+still_status still_compact_layer(const still_config *cfg, const still_layer_weights *w,
+                                 const void *K, const void *V, const double *positions,
+                                 int64_t N, double rope_theta, int32_t t, uint32_t flags,
+                                 void *C_k, void *C_v, double *out_positions,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+
+/* Compact n_layers independent layers (Appendix A, per-layer stack) that share
+ * one position vector.  w, K, V, C_k, C_v are HOST arrays of n_layers entries
+ * (each entry a device pointer, or a struct of device pointers for w). */
+still_status still_compact_model(const still_config *cfg, int32_t n_layers,
+                                 const still_layer_weights *w,
+                                 const void *const *K, const void *const *V,
+                                 const double *positions, int64_t N, double rope_theta,
+                                 int32_t t, uint32_t flags,
+                                 void *const *C_k, void *const *C_v, double *out_positions,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+
+/* Human-readable name of a status code (static string). */
+const char *still_status_string(int32_t status);
+
+/* Detail of the last non-OK status returned on the calling thread. */
+const char *still_last_error(void);
+
+/* Library version string. */
+const char *still_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* STILL_H_ */

@@ -1,0 +1,222 @@
+"""ctypes binding of libstill.so (include/still.h).
+
+Argument marshalling only: torch tensors supply device pointers and the
+current HIP stream; every step of the compaction runs in the library's HIP
+kernels.  There is no fallback: if the library is missing or fails to load,
+every entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence
+
+from . import configs
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstill.so")
+
+STILL_OK = 0
+STATUS = {0: "STILL_OK", -1: "STILL_E_INVAL", -2: "STILL_E_SHAPE", -3: "STILL_E_DTYPE",
+          -4: "STILL_E_WORKSPACE", -5: "STILL_E_UNSUPPORTED", -6: "STILL_E_HIP"}
+STILL_F_REROTATE = 1
+
+
+class StillError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+        self.status = status
+
+
+class still_config(ctypes.Structure):
+    _fields_ = [("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("latent_dim", ctypes.c_int32), ("n_blocks", ctypes.c_int32),
+                ("cross_every_block", ctypes.c_int32), ("n_cross_heads", ctypes.c_int32),
+                ("cross_head_dim", ctypes.c_int32), ("n_self_heads", ctypes.c_int32),
+                ("self_head_dim", ctypes.c_int32), ("ffn_kind", ctypes.c_int32),
+                ("ffn_hidden", ctypes.c_int32), ("final_norm", ctypes.c_int32),
+                ("logit_scale_cross", ctypes.c_float), ("logit_scale_self", ctypes.c_float),
+                ("compactor_rope_base", ctypes.c_double), ("rms_eps", ctypes.c_float),
+                ("l2_eps", ctypes.c_float), ("mode", ctypes.c_int32)]
+
+
+_BLOCK_FIELDS = ["ca_wq", "ca_bq", "ca_wk", "ca_bk", "ca_wv", "ca_wo",
+                 "sa_wq", "sa_bq", "sa_wk", "sa_bk", "sa_wv", "sa_wo",
+                 "ffn_wg", "ffn_wu", "ffn_wd"]
+
+
+class still_block_weights(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_void_p) for f in _BLOCK_FIELDS]
+
+
+class still_layer_weights(ctypes.Structure):
+    _fields_ = [("latents", ctypes.c_void_p), ("t_bank", ctypes.c_int32),
+                ("blocks", ctypes.POINTER(still_block_weights)),
+                ("w_key", ctypes.c_void_p), ("w_val", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libstill.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2606_07878_amd.build` (no CPU fallback exists)")
+        L = ctypes.CDLL(_LIB_PATH)
+        L.still_workspace_size.argtypes = [ctypes.POINTER(still_config), ctypes.c_int64, ctypes.c_int32,
+                                           ctypes.c_int32]
+        L.still_workspace_size.restype = ctypes.c_size_t
+        common = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_double, ctypes.c_int32, ctypes.c_uint32]
+        L.still_compact_layer.argtypes = [ctypes.POINTER(still_config), ctypes.POINTER(still_layer_weights),
+                                          ctypes.c_void_p, ctypes.c_void_p, *common,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.still_compact_layer.restype = ctypes.c_int32
+        L.still_compact_model.argtypes = [ctypes.POINTER(still_config), ctypes.c_int32,
+                                          ctypes.POINTER(still_layer_weights),
+                                          ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_void_p),
+                                          *common,
+                                          ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_void_p),
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.still_compact_model.restype = ctypes.c_int32
+        L.still_status_string.argtypes = [ctypes.c_int32]
+        L.still_status_string.restype = ctypes.c_char_p
+        L.still_last_error.argtypes = []
+        L.still_last_error.restype = ctypes.c_char_p
+        L.still_version.argtypes = []
+        L.still_version.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def make_config(cfg: configs.CompactorConfig, mode: int = configs.MODE_BF16) -> still_config:
+    return still_config(cfg.n_kv_heads, cfg.head_dim, cfg.latent_dim, cfg.n_blocks, cfg.cross_every_block,
+                        cfg.n_cross_heads, cfg.cross_head_dim, cfg.n_self_heads, cfg.self_head_dim,
+                        cfg.ffn_kind, cfg.ffn_hidden, cfg.final_norm, cfg.logit_scale_cross,
+                        cfg.logit_scale_self, cfg.compactor_rope_base, cfg.rms_eps, cfg.l2_eps, mode)
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    return x.data_ptr() if hasattr(x, "data_ptr") else int(x)
+
+
+class LayerWeights:
+    """still_layer_weights built from a dict of device tensors keyed like
+    ``configs.layer_shapes`` (keeps the tensors alive)."""
+
+    def __init__(self, cfg: configs.CompactorConfig, tensors: Dict[str, object]):
+        self.tensors = tensors
+        nb = cfg.n_blocks
+        self._blocks = (still_block_weights * nb)()
+        for b in range(nb):
+            for f in _BLOCK_FIELDS:
+                setattr(self._blocks[b], f, _ptr(tensors.get(f"b{b}.{f}")))
+        lat = tensors["latents"]
+        self.struct = still_layer_weights(_ptr(lat), int(lat.shape[1]), self._blocks,
+                                          _ptr(tensors["w_key"]), _ptr(tensors["w_val"]))
+
+
+def _check(status: int):
+    if status != STILL_OK:
+        raise StillError(status, lib().still_last_error().decode())
+
+
+def still_workspace_size(cfg: still_config, N: int, t: int, n_layers: int = 1) -> int:
+    return int(lib().still_workspace_size(ctypes.byref(cfg), N, t, n_layers))
+
+
+def still_compact_layer(cfg: still_config, w: LayerWeights, K, V, positions, N: int, rope_theta: float,
+                        t: int, flags: int, C_k, C_v, out_positions, workspace, workspace_bytes: int,
+                        stream) -> int:
+    """Raw entry point (pointers or tensors); returns the status code."""
+    return lib().still_compact_layer(ctypes.byref(cfg), ctypes.byref(w.struct), _ptr(K), _ptr(V),
+                                     _ptr(positions), N, rope_theta, t, flags, _ptr(C_k), _ptr(C_v),
+                                     _ptr(out_positions), _ptr(workspace), workspace_bytes, _ptr(stream))
+
+
+def still_compact_model(cfg: still_config, ws: Sequence[LayerWeights], K: Sequence, V: Sequence, positions,
+                        N: int, rope_theta: float, t: int, flags: int, C_k: Sequence, C_v: Sequence,
+                        out_positions, workspace, workspace_bytes: int, stream) -> int:
+    L = len(ws)
+    wa = (still_layer_weights * L)(*[w.struct for w in ws])
+    arr = lambda xs: (ctypes.c_void_p * L)(*[_ptr(x) for x in xs])  # noqa: E731
+    return lib().still_compact_model(ctypes.byref(cfg), L, wa, arr(K), arr(V), _ptr(positions), N,
+                                     rope_theta, t, flags, arr(C_k), arr(C_v), _ptr(out_positions),
+                                     _ptr(workspace), workspace_bytes, _ptr(stream))
+
+
+def still_status_string(status: int) -> str:
+    return lib().still_status_string(status).decode()
+
+
+def still_last_error() -> str:
+    return lib().still_last_error().decode()
+
+
+def still_version() -> str:
+    return lib().still_version().decode()
+
+
+# ----------------------------------------------------------------------------
+# torch conveniences (allocation of outputs / workspace on the caller's device)
+# ----------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def compact_model(cfg: configs.CompactorConfig, weights: List[Dict[str, object]], K: List, V: List, positions,
+                  rope_theta: float, t: int, rerotate: bool = True, mode: int = configs.MODE_BF16,
+                  workspace=None, outputs=None):
+    """Compact L layers on the current stream; returns ([C_k], [C_v], out_positions)."""
+    torch = _torch()
+    dev = K[0].device
+    ccfg = make_config(cfg, mode)
+    N = int(K[0].shape[1])
+    L = len(K)
+    need = still_workspace_size(ccfg, N, t, L)
+    if need == 0:
+        raise StillError(-5, "configuration rejected by still_workspace_size")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    dt = K[0].dtype
+    if outputs is None:
+        Ck = [torch.empty(cfg.n_kv_heads, t, cfg.head_dim, dtype=dt, device=dev) for _ in range(L)]
+        Cv = [torch.empty(cfg.n_kv_heads, t, cfg.head_dim, dtype=dt, device=dev) for _ in range(L)]
+    else:
+        Ck, Cv = outputs
+    outp = torch.empty(t, dtype=torch.float64, device=dev)
+    lw = [w if isinstance(w, LayerWeights) else LayerWeights(cfg, w) for w in weights]
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(still_compact_model(ccfg, lw, K, V, positions, N, rope_theta, t,
+                               STILL_F_REROTATE if rerotate else 0, Ck, Cv, outp, workspace,
+                               workspace.numel(), stream))
+    return Ck, Cv, outp
+
+
+def compact_layer(cfg: configs.CompactorConfig, weights: Dict[str, object], K, V, positions, rope_theta: float,
+                  t: int, rerotate: bool = True, mode: int = configs.MODE_BF16, workspace=None):
+    """Compact one layer through still_compact_layer; returns (C_k, C_v, out_positions)."""
+    torch = _torch()
+    dev = K.device
+    ccfg = make_config(cfg, mode)
+    N = int(K.shape[1])
+    need = still_workspace_size(ccfg, N, t, 1)
+    if need == 0:
+        raise StillError(-5, "configuration rejected by still_workspace_size")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    Ck = torch.empty(cfg.n_kv_heads, t, cfg.head_dim, dtype=K.dtype, device=dev)
+    Cv = torch.empty_like(Ck)
+    outp = torch.empty(t, dtype=torch.float64, device=dev)
+    lw = weights if isinstance(weights, LayerWeights) else LayerWeights(cfg, weights)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(still_compact_layer(ccfg, lw, K, V, positions, N, rope_theta, t,
+                               STILL_F_REROTATE if rerotate else 0, Ck, Cv, outp, workspace,
+                               workspace.numel(), stream))
+    return Ck, Cv, outp

@@ -1,0 +1,240 @@
+// attn.hpp - flash-style latent -> cache cross-attention (one KV head h, one
+// cross head c per grid row), split over the key axis.
+//
+// For a tile of TT latents and a key range, stream key blocks of NB keys:
+//   S^T = K_blk Q^T              (contraction over the head width, MFMA)
+//   logits = S^T * rk[key] * rq[lat] * s * log2(e)   (QK-norm folded in)
+//   online softmax over keys (running max m, running sum l per latent)
+//   O^T += X_blk^T P^T           (contraction over the block's keys, MFMA)
+// and write the un-normalised partial (O, m, l) of the key range.  The value
+// projection W_V is applied afterwards to the merged O = P X (exact
+// re-association of P (X W_V)).
+//
+// Orientation: keys are MFMA rows and latents MFMA columns in the first
+// product, so every lane owns one latent and the softmax statistics stay in
+// the lane; the S^T accumulator is then already a valid B operand of the
+// second product once the block's keys are read from X^T in the matching
+// (permuted) order.
+#pragma once
+#include "common.hpp"
+
+namespace still {
+
+struct AttnArgs {
+  const void* q;     // [H*t][nc*dc]  rotated, un-normalised queries (CT)
+  long ldq;
+  const float* rq;   // [H*t][nc]     1 / max(||q~||, eps)
+  const void* k;     // [H*N][nc*dc]  rotated, un-normalised keys (CT)
+  long ldk;
+  const float* rk;   // [H*N][nc]
+  const void* xt;    // [H][2d][ldxt] X^T (CT), zero beyond N up to ldxt
+  long ldxt;
+  float* opart;      // [S][H*nc][t][2d]
+  float* mpart;      // [S][H*nc][t]
+  float* lpart;      // [S][H*nc][t]
+  int H, N, t, nc, dc, d2;
+  float scale_log2;  // logit scale * log2(e)
+  int keys_per_split;
+};
+
+template <class CT, int TT, int NB, int DK, int D2>
+__global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
+  typedef Mma<CT> MM;
+  typedef typename MM::frag frag;
+  constexpr int E = MM::E;
+  constexpr int PAD = 16 / sizeof(CT);
+  constexpr int LQ = DK + PAD;           // Q/K stage row stride
+  constexpr int LX = NB + PAD;           // X^T block row stride
+  constexpr int KT = NB / 32;            // key tiles per block
+  constexpr int FT = D2 / 32;            // feature tiles
+  constexpr int QV = TT * DK / E / 256;  // stage vectors per thread
+  constexpr int KVv = NB * DK / E / 256;
+  constexpr int XV = D2 * NB / E / 256;
+  static_assert(TT == 128, "4 waves x 32 latents");
+  static_assert(QV >= 1 && KVv >= 1 && XV >= 1, "tile sizes");
+
+  __shared__ __attribute__((aligned(16))) CT Qs[2][TT * LQ];
+  __shared__ __attribute__((aligned(16))) CT Ks[2][NB * LQ];
+  __shared__ __attribute__((aligned(16))) CT Xs[D2 * LX];
+  __shared__ float rks[NB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, lg = lane >> 5;
+  const int hc = blockIdx.y, h = hc / a.nc, c = hc - h * a.nc;
+  const int t0 = blockIdx.x * TT;
+  const int split = blockIdx.z;
+  const int nbeg = split * a.keys_per_split;
+  const int nend = min(a.N, nbeg + a.keys_per_split);
+
+  const CT* qbase = (const CT*)a.q + (long)h * a.t * a.ldq + (long)c * a.dc;
+  const CT* kbase = (const CT*)a.k + (long)h * a.N * a.ldk + (long)c * a.dc;
+  const CT* xtb = (const CT*)a.xt + (long)h * a.d2 * a.ldxt;
+  const float* rkb = a.rk + (long)h * a.N * a.nc + c;
+
+  const int my_lat = t0 + wave * 32 + l32;
+  const float rq = my_lat < a.t ? a.rq[((long)h * a.t + my_lat) * a.nc + c] : 0.f;
+  const float qscale = rq * a.scale_log2;
+
+  f32x16 o[FT];
+#pragma unroll
+  for (int f = 0; f < FT; ++f) o[f] = zero16();
+  float m_run = -INFINITY, l_run = 0.f;
+
+  frag rq_[QV], rk_[KVv], rx[XV];
+  auto load_qk = [&](int n0, int d0) {
+#pragma unroll
+    for (int i = 0; i < QV; ++i) {
+      const int v = tid + i * 256, r = v / (DK / E), kk = (v % (DK / E)) * E;
+      const int lat = t0 + r;
+      rq_[i] = lat < a.t ? *(const frag*)(qbase + (long)lat * a.ldq + d0 + kk) : zero_frag<CT>();
+    }
+#pragma unroll
+    for (int i = 0; i < KVv; ++i) {
+      const int v = tid + i * 256, r = v / (DK / E), kk = (v % (DK / E)) * E;
+      const int n = n0 + r;
+      rk_[i] = n < nend ? *(const frag*)(kbase + (long)n * a.ldk + d0 + kk) : zero_frag<CT>();
+    }
+  };
+  auto store_qk = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < QV; ++i) {
+      const int v = tid + i * 256, r = v / (DK / E), kk = (v % (DK / E)) * E;
+      *(frag*)&Qs[buf][r * LQ + kk] = rq_[i];
+    }
+#pragma unroll
+    for (int i = 0; i < KVv; ++i) {
+      const int v = tid + i * 256, r = v / (DK / E), kk = (v % (DK / E)) * E;
+      *(frag*)&Ks[buf][r * LQ + kk] = rk_[i];
+    }
+  };
+  auto load_x = [&](int n0) {
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int v = tid + i * 256, f = v / (NB / E), kk = (v % (NB / E)) * E;
+      rx[i] = *(const frag*)(xtb + (long)f * a.ldxt + n0 + kk);   // padded: always in bounds
+    }
+  };
+
+  const int nd = a.dc / DK;
+  for (int n0 = nbeg; n0 < nend; n0 += NB) {
+    // ---- S^T = K_blk Q^T over the head width
+    f32x16 s[KT];
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) s[kt] = zero16();
+    load_x(n0);
+    load_qk(n0, 0);
+    store_qk(0);
+    __syncthreads();
+    for (int di = 0; di < nd; ++di) {
+      const int cur = di & 1;
+      if (di + 1 < nd) load_qk(n0, (di + 1) * DK);
+#pragma unroll
+      for (int ks = 0; ks < DK / (2 * E); ++ks) {
+        const frag bq = *(const frag*)&Qs[cur][(wave * 32 + l32) * LQ + ks * 2 * E + lg * E];
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) {
+          const frag ak = *(const frag*)&Ks[cur][(kt * 32 + l32) * LQ + ks * 2 * E + lg * E];
+          MM::mma(s[kt], ak, bq);
+        }
+      }
+      if (di + 1 < nd) store_qk(cur ^ 1);
+      __syncthreads();
+    }
+    // ---- stage X^T block and the key norms
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int v = tid + i * 256, f = v / (NB / E), kk = (v % (NB / E)) * E;
+      *(frag*)&Xs[f * LX + kk] = rx[i];
+    }
+    if (tid < NB) {
+      const int n = n0 + tid;
+      rks[tid] = n < nend ? rkb[(long)n * a.nc] : 0.f;
+    }
+    __syncthreads();
+
+    // ---- online softmax (lane owns latent my_lat; keys in registers)
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int kl = kt * 32 + 8 * (j >> 2) + 4 * lg + (j & 3);
+        float x = s[kt][j] * rks[kl] * qscale;
+        x = (n0 + kl < nend) ? x : -INFINITY;
+        s[kt][j] = x;
+        mx = fmaxf(mx, x);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const float p = (m_new == -INFINITY) ? 0.f : exp2f(s[kt][j] - m_new);
+        s[kt][j] = p;
+        psum += p;
+      }
+    psum += __shfl_xor(psum, 32);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int f = 0; f < FT; ++f)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) o[f][j] *= alpha;
+
+    // ---- O^T += X^T P^T
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      if constexpr (E == 8) {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          half8 bp;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) bp[e] = (f16)s[kt][8 * hf + e];
+          const int key0 = kt * 32 + 16 * hf + 4 * lg;   // keys key0..+3 and key0+8..+11
+#pragma unroll
+          for (int f = 0; f < FT; ++f) {
+            const CT* xr = &Xs[(f * 32 + l32) * LX];
+            const half4 lo = *(const half4*)(xr + key0);
+            const half4 hi = *(const half4*)(xr + key0 + 8);
+            half8 ax;
+            ax[0] = lo[0]; ax[1] = lo[1]; ax[2] = lo[2]; ax[3] = lo[3];
+            ax[4] = hi[0]; ax[5] = hi[1]; ax[6] = hi[2]; ax[7] = hi[3];
+            MM::mma(o[f], *(const frag*)&ax, *(const frag*)&bp);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          frag bp;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) bp[e] = s[kt][4 * qd + e];
+          const int key0 = kt * 32 + 8 * qd + 4 * lg;     // keys key0..+3
+#pragma unroll
+          for (int f = 0; f < FT; ++f) {
+            const frag ax = *(const frag*)&Xs[(f * 32 + l32) * LX + key0];
+            MM::mma(o[f], ax, bp);
+          }
+        }
+      }
+    }
+  }
+
+  // ---- write the partial (O un-normalised, m, l) of this key range
+  if (my_lat < a.t) {
+    const long row = ((long)split * a.H * a.nc + hc) * a.t + my_lat;
+    float* op = a.opart + row * a.d2;
+#pragma unroll
+    for (int f = 0; f < FT; ++f)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) op[f * 32 + 8 * (j >> 2) + 4 * lg + (j & 3)] = o[f][j];
+    if (lg == 0) {
+      a.mpart[row] = m_run;
+      a.lpart[row] = l_run;
+    }
+  }
+}
+
+}  // namespace still

@@ -1,0 +1,123 @@
+// common.hpp - element types, conversions and the CDNA4 MFMA step used by
+// every kernel of the compactor library (gfx950 only).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace still {
+
+typedef _Float16 f16;
+typedef f16 half8 __attribute__((ext_vector_type(8)));
+typedef f16 half4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// bfloat16 held as raw bits (I/O type of the bf16 mode).
+struct bf16 {
+  uint16_t x;
+};
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(f16 v) { return (float)v; }
+__device__ __forceinline__ float to_f32(bf16 v) { return __uint_as_float((uint32_t)v.x << 16); }
+
+// float -> bfloat16, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ bf16 f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  bf16 r;
+  if ((u & 0x7fffffffu) > 0x7f800000u) {
+    r.x = (uint16_t)((u >> 16) | 0x40u);
+  } else {
+    u += 0x7fffu + ((u >> 16) & 1u);
+    r.x = (uint16_t)(u >> 16);
+  }
+  return r;
+}
+
+template <class T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ f16 from_f32<f16>(float v) { return (f16)v; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return f32_to_bf16(v); }
+
+// ---------------------------------------------------------------------------
+// MFMA step on 32x32 output tiles.  A "fragment" is the 16 bytes one lane
+// contributes per step: lanes 0-31 hold k in [0,E), lanes 32-63 k in [E,2E)
+// of a 2E-wide k chunk, for row (A) or column (B) lane%32.
+//  * f16: one v_mfma_f32_32x32x16_f16 (E = 8, k chunk 16).
+//  * f32: four v_mfma_f32_32x32x2_f32, component s of both operands forming
+//    the k pair (s, E+s); any fixed pairing sums every k exactly once.
+// Output layout (both): lane l, register j -> row 8*(j/4) + 4*(l/32) + j%4,
+// column l%32.
+// ---------------------------------------------------------------------------
+template <class CT> struct Mma;
+
+template <> struct Mma<f16> {
+  typedef half8 frag;
+  static constexpr int E = 8;
+  static __device__ __forceinline__ void mma(f32x16& c, const frag& a, const frag& b) {
+    c = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <> struct Mma<float> {
+  typedef f32x4 frag;
+  static constexpr int E = 4;
+  static __device__ __forceinline__ void mma(f32x16& c, const frag& a, const frag& b) {
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[1], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[2], b[2], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[3], b[3], c, 0, 0, 0);
+  }
+};
+
+// Load E consecutive elements of type T (16-byte aligned run) as a CT fragment.
+template <class CT, class T> struct VecLoad;
+
+template <> struct VecLoad<f16, f16> {
+  static __device__ __forceinline__ half8 load(const f16* p) { return *(const half8*)p; }
+};
+template <> struct VecLoad<f16, bf16> {
+  static __device__ __forceinline__ half8 load(const bf16* p) {
+    uint4 u = *(const uint4*)p;
+    half8 r;
+    uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r[2 * i] = (f16)__uint_as_float(w[i] << 16);
+      r[2 * i + 1] = (f16)__uint_as_float(w[i] & 0xffff0000u);
+    }
+    return r;
+  }
+};
+template <> struct VecLoad<f16, float> {
+  static __device__ __forceinline__ half8 load(const float* p) {
+    f32x4 a = *(const f32x4*)p;
+    f32x4 b = *(const f32x4*)(p + 4);
+    half8 r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      r[i] = (f16)a[i];
+      r[4 + i] = (f16)b[i];
+    }
+    return r;
+  }
+};
+template <> struct VecLoad<float, float> {
+  static __device__ __forceinline__ f32x4 load(const float* p) { return *(const f32x4*)p; }
+};
+
+template <class CT> __device__ __forceinline__ typename Mma<CT>::frag zero_frag() {
+  typename Mma<CT>::frag z;
+#pragma unroll
+  for (int i = 0; i < Mma<CT>::E; ++i) z[i] = (CT)0;
+  return z;
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+}  // namespace still

@@ -1,0 +1,612 @@
+// still.hip - C ABI (include/still.h) of the Still compactor forward pass on
+// MI355X: argument validation, workspace planning and the per-layer launch
+// sequence of the HIP kernels in gemm.hpp, attn.hpp and misc.hpp.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "../../include/still.h"
+#include "attn.hpp"
+#include "common.hpp"
+#include "gemm.hpp"
+#include "misc.hpp"
+
+namespace still {
+
+static thread_local std::string g_last_error;
+
+static still_status fail(still_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+#define HIP_TRY(expr)                                                                         \
+  do {                                                                                        \
+    hipError_t _e = (expr);                                                                   \
+    if (_e != hipSuccess) return fail(STILL_E_HIP, "%s: %s", #expr, hipGetErrorString(_e));   \
+  } while (0)
+
+static inline long rup(long x, long m) { return (x + m - 1) / m * m; }
+
+constexpr int GEMM_BN = 128;   // column tile of every GEMM (two halves of 64 pairs)
+constexpr int ATT_TT = 128;    // latents per attention workgroup
+constexpr int ATT_NB = 64;     // keys per attention block
+
+// ---------------------------------------------------------------------------
+// Derived dimensions and workspace layout
+// ---------------------------------------------------------------------------
+struct Dims {
+  int H, d, D, d2, nc, dc, ns, ds, F, Ec, Es, t, tpad;
+  long N, Npad;
+  int np_c, np_s;       // sum-of-squares partials per (row, head)
+  int splits;           // split-N factor of the cross-attention
+  long keys_per_split;
+  size_t cs;            // bytes of the compute/storage type
+  bool fp32;
+};
+
+struct Plan {
+  size_t pq, tab_ck, tab_cq, tab_bk, tab_bq;
+  size_t X, XT, Z, Y, q, partq, rq, O;
+  // union region: cross-attention key side ...
+  size_t k, partk, rk, opart, mpart, lpart;
+  // ... or self-attention / FFN buffers
+  size_t qs, ks, vT, partqs, partks, rqs, rks, Ssa, Psa, Osa, hid;
+  size_t total;
+};
+
+static int choose_splits(const Dims& m) {
+  const long wgs = (long)((m.t + ATT_TT - 1) / ATT_TT) * m.H * m.nc;
+  const long nblocks = (m.N + ATT_NB - 1) / ATT_NB;
+  long s = (1024 + wgs - 1) / wgs;            // aim for >= 4 workgroups per CU
+  if (s > nblocks) s = nblocks;
+  if (s < 1) s = 1;
+  return (int)s;
+}
+
+static still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims* m) {
+  if (!c) return fail(STILL_E_INVAL, "config is NULL");
+  if (c->mode != STILL_MODE_BF16 && c->mode != STILL_MODE_FP32) return fail(STILL_E_DTYPE, "unknown mode %d", c->mode);
+  if (c->n_kv_heads < 1 || c->head_dim < 2 || c->latent_dim < 1 || c->n_blocks < 1)
+    return fail(STILL_E_INVAL, "non-positive dimension in config");
+  if (N < 1 || t < 1) return fail(STILL_E_INVAL, "N and t must be >= 1 (N=%lld t=%d)", (long long)N, t);
+  if (c->head_dim % 2) return fail(STILL_E_SHAPE, "head_dim must be even (got %d)", c->head_dim);
+  if (c->n_cross_heads < 1) return fail(STILL_E_INVAL, "n_cross_heads must be >= 1");
+  if (c->n_self_heads < 0) return fail(STILL_E_INVAL, "n_self_heads must be >= 0");
+  if (c->ffn_kind < 0 || c->ffn_kind > 2) return fail(STILL_E_INVAL, "unknown ffn_kind %d", c->ffn_kind);
+  if (c->ffn_kind != STILL_FFN_NONE && c->ffn_hidden < 1) return fail(STILL_E_INVAL, "ffn_hidden must be >= 1");
+  if (!(c->compactor_rope_base > 0.0)) return fail(STILL_E_INVAL, "compactor_rope_base must be > 0");
+  if (!(c->l2_eps > 0.f) || !(c->rms_eps >= 0.f)) return fail(STILL_E_INVAL, "eps must be positive");
+  m->H = c->n_kv_heads;
+  m->d = c->head_dim;
+  m->D = c->latent_dim;
+  m->d2 = 2 * m->d;
+  m->nc = c->n_cross_heads;
+  m->dc = c->cross_head_dim ? c->cross_head_dim : c->latent_dim;
+  m->ns = c->n_self_heads;
+  m->ds = c->self_head_dim ? c->self_head_dim : c->latent_dim;
+  m->F = c->ffn_kind ? c->ffn_hidden : 0;
+  m->Ec = m->nc * m->dc;
+  m->Es = m->ns * m->ds;
+  m->t = t;
+  m->N = N;
+  m->fp32 = c->mode == STILL_MODE_FP32;
+  m->cs = m->fp32 ? 4 : 2;
+  // kernel-imposed limits
+  if (m->d != 64 && m->d != 128 && m->d != 256)
+    return fail(STILL_E_UNSUPPORTED, "head_dim %d unsupported (64, 128 or 256)", m->d);
+  if (m->dc % GEMM_BN) return fail(STILL_E_UNSUPPORTED, "cross head width %d must be a multiple of %d", m->dc, GEMM_BN);
+  if (m->ns > 0 && m->ds % GEMM_BN)
+    return fail(STILL_E_UNSUPPORTED, "self head width %d must be a multiple of %d", m->ds, GEMM_BN);
+  if (m->D % 8) return fail(STILL_E_UNSUPPORTED, "latent_dim %d must be a multiple of 8", m->D);
+  if (m->F % 8) return fail(STILL_E_UNSUPPORTED, "ffn_hidden %d must be a multiple of 8", m->F);
+  if ((long)m->H * N > (long)GEMM_BN * 65535L)
+    return fail(STILL_E_UNSUPPORTED, "H*N = %lld exceeds the supported %ld rows", (long long)(m->H * N), (long)GEMM_BN * 65535L);
+  m->tpad = (int)rup(t, 64);
+  m->Npad = rup(N, 128);
+  m->np_c = m->dc / GEMM_BN * 2;
+  m->np_s = m->ns > 0 ? m->ds / GEMM_BN * 2 : 0;
+  m->splits = choose_splits(*m);
+  m->keys_per_split = rup((m->N + m->splits - 1) / m->splits, ATT_NB);
+  m->splits = (int)((m->N + m->keys_per_split - 1) / m->keys_per_split);
+  return STILL_OK;
+}
+
+static Plan make_plan(const Dims& m) {
+  Plan p;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += (bytes + 255) & ~(size_t)255;
+    return o;
+  };
+  const size_t cs = m.cs;
+  const long Ht = (long)m.H * m.t;
+  const long HN = (long)m.H * m.N;
+  p.pq = take(sizeof(double) * m.t);
+  p.tab_ck = take(8ul * m.N * (m.dc / 2));
+  p.tab_cq = take(8ul * m.t * (m.dc / 2));
+  p.tab_bk = take(8ul * m.N * (m.d / 2));
+  p.tab_bq = take(8ul * m.t * (m.d / 2));
+  p.X = take(cs * HN * m.d2);
+  p.XT = take(cs * (size_t)m.H * m.d2 * m.Npad);
+  p.Z = take(4ul * Ht * m.D);
+  p.Y = take(cs * Ht * m.D);
+  p.q = take(cs * Ht * m.Ec);            // also the cross-attention head outputs
+  p.partq = take(4ul * Ht * m.nc * m.np_c);
+  p.rq = take(4ul * Ht * m.nc);
+  p.O = take(cs * Ht * m.nc * m.d2);
+  const size_t ubase = off;
+  p.k = take(cs * HN * m.Ec);
+  p.partk = take(4ul * HN * m.nc * m.np_c);
+  p.rk = take(4ul * HN * m.nc);
+  p.opart = take(4ul * m.splits * Ht * m.nc * m.d2);
+  p.mpart = take(4ul * m.splits * Ht * m.nc);
+  p.lpart = take(4ul * m.splits * Ht * m.nc);
+  const size_t end1 = off;
+  off = ubase;
+  if (m.ns > 0) {
+    p.qs = take(cs * Ht * m.Es);
+    p.ks = take(cs * Ht * m.Es);
+    p.vT = take(cs * (size_t)m.H * m.Es * m.tpad);
+    p.partqs = take(4ul * Ht * m.ns * m.np_s);
+    p.partks = take(4ul * Ht * m.ns * m.np_s);
+    p.rqs = take(4ul * Ht * m.ns);
+    p.rks = take(4ul * Ht * m.ns);
+    p.Ssa = take(4ul * (size_t)m.H * m.ns * m.t * m.tpad);
+    p.Psa = take(cs * (size_t)m.H * m.ns * m.t * m.tpad);
+    p.Osa = take(cs * Ht * m.Es);
+  }
+  p.hid = take(cs * Ht * (m.F > 0 ? m.F : 1));
+  p.total = (off > end1 ? off : end1) + 256;
+  return p;
+}
+
+// ---------------------------------------------------------------------------
+// Launch helpers
+// ---------------------------------------------------------------------------
+template <class CT> struct Tile;
+template <> struct Tile<f16> { static constexpr int BM = 128, BN = GEMM_BN, BK = 32; };
+template <> struct Tile<float> { static constexpr int BM = 128, BN = GEMM_BN, BK = 16; };
+
+template <class CT, class TA, class TB, class TC, class TBias, int EPI>
+static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st) {
+  return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
+}
+
+static GemmArgs gargs(int M, int N, int K, const void* A, long lda, const void* B, long ldb, void* C, long ldc) {
+  GemmArgs g;
+  memset(&g, 0, sizeof g);
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.nb2 = 1;
+  g.A = A;
+  g.lda = lda;
+  g.B = B;
+  g.ldb = ldb;
+  g.C = C;
+  g.ldc = ldc;
+  return g;
+}
+
+static inline int grid1d(long n, int per = 256) {
+  long b = (n + per - 1) / per;
+  if (b > 65535L * 16) b = 65535L * 16;
+  if (b < 1) b = 1;
+  return (int)b;
+}
+
+template <class CT, int D2>
+static hipError_t launch_attn(const AttnArgs& a, int splits, hipStream_t st) {
+  dim3 grid((a.t + ATT_TT - 1) / ATT_TT, a.H * a.nc, splits);
+  if constexpr (sizeof(CT) == 2) {
+    hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, ATT_NB, 64, D2>), grid, dim3(256), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, (D2 > 256 ? 32 : ATT_NB), 32, D2>), grid, dim3(256), 0, st, a);
+  }
+  return hipGetLastError();
+}
+
+// per-call tables shared by all layers
+static still_status prepare_tables(const Dims& m, const Plan& p, char* ws, const double* positions,
+                                   double rope_theta, double cbase, bool rerotate, double* out_positions,
+                                   hipStream_t st) {
+  double* pq = (double*)(ws + p.pq);
+  hipLaunchKernelGGL(positions_kernel, dim3(1), dim3(256), 0, st, positions, m.N, m.t, pq, out_positions);
+  HIP_TRY(hipGetLastError());
+  auto table = [&](const double* pos, long R, int w, double base, size_t off) -> hipError_t {
+    hipLaunchKernelGGL(rope_table_kernel, dim3(grid1d(R * (w / 2))), dim3(256), 0, st, pos, R, w, base,
+                       (float2*)(ws + off));
+    return hipGetLastError();
+  };
+  HIP_TRY(table(positions, m.N, m.dc, cbase, p.tab_ck));
+  HIP_TRY(table(pq, m.t, m.dc, cbase, p.tab_cq));
+  HIP_TRY(table(positions, m.N, m.d, rope_theta, p.tab_bk));
+  if (rerotate) HIP_TRY(table(pq, m.t, m.d, rope_theta, p.tab_bq));
+  return STILL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// One layer: IT = I/O type of K, V, weights and outputs; CT = MFMA operand /
+// intermediate storage type.
+// ---------------------------------------------------------------------------
+template <class IT, class CT>
+static still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, char* ws,
+                              const still_layer_weights* w, const void* Kp, const void* Vp, bool rerotate,
+                              void* Ckp, void* Cvp, hipStream_t st) {
+  const long Ht = (long)m.H * m.t;
+  const long HN = (long)m.H * m.N;
+  CT* X = (CT*)(ws + p.X);
+  CT* XT = (CT*)(ws + p.XT);
+  float* Z = (float*)(ws + p.Z);
+  CT* Y = (CT*)(ws + p.Y);
+  CT* q = (CT*)(ws + p.q);
+  CT* head = q;
+  float* partq = (float*)(ws + p.partq);
+  float* rq = (float*)(ws + p.rq);
+  CT* O = (CT*)(ws + p.O);
+  CT* k = (CT*)(ws + p.k);
+  float* partk = (float*)(ws + p.partk);
+  float* rk = (float*)(ws + p.rk);
+  const float2* tab_ck = (const float2*)(ws + p.tab_ck);
+  const float2* tab_cq = (const float2*)(ws + p.tab_cq);
+  const float2* tab_bk = (const float2*)(ws + p.tab_bk);
+  const float2* tab_bq = (const float2*)(ws + p.tab_bq);
+  const float LOG2E = 1.4426950408889634f;
+
+  // RoPE-fix staging of X = [R(-p) K ; V] and X^T
+  {
+    int RW = 64;
+    while (RW > 8 && (size_t)RW * (m.d2 + 1) * m.cs > 32768) RW /= 2;
+    const size_t lds = (size_t)RW * (m.d2 + 1) * m.cs;
+    dim3 grid((unsigned)((m.Npad + RW - 1) / RW), m.H);
+    hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, tab_bk, m.N,
+                       m.d, X, XT, m.Npad, RW);
+    HIP_TRY(hipGetLastError());
+  }
+  hipLaunchKernelGGL((init_z_kernel<IT>), dim3(grid1d(Ht * m.D)), dim3(256), 0, st, (const IT*)w->latents, Z, Ht * m.D);
+  HIP_TRY(hipGetLastError());
+  auto rmsnorm = [&]() -> hipError_t {
+    hipLaunchKernelGGL((rmsnorm_kernel<CT>), dim3((unsigned)((Ht + 3) / 4)), dim3(256), 0, st, Z, Y, Ht, m.D,
+                       cfg->rms_eps);
+    return hipGetLastError();
+  };
+  auto finalize = [&](const float* part, long rows, int nh, int np, float* rn) -> hipError_t {
+    hipLaunchKernelGGL(finalize_norm_kernel, dim3(grid1d(rows * nh)), dim3(256), 0, st, part, rows, nh, np,
+                       cfg->l2_eps, rn);
+    return hipGetLastError();
+  };
+
+  for (int b = 0; b < cfg->n_blocks; ++b) {
+    const still_block_weights& bw = w->blocks[b];
+    // ---------------- cross-attention: Z += CrossAttn(RMSNorm(Z), X)
+    if (cfg->cross_every_block || b == 0) {
+      HIP_TRY(rmsnorm());
+      {  // q = RoPE_c(q~) with q~ = Y W_Q^T + b_Q, plus ||q~||^2 partials
+        GemmArgs g = gargs((int)Ht, m.Ec / 2, m.D, Y, m.D, bw.ca_wq, m.D, q, m.Ec);
+        g.bias = bw.ca_bq;
+        g.hd = m.dc;
+        g.tab = tab_cq;
+        g.tab_mod = m.t;
+        g.part = partq;
+        g.ldpart = (long)m.nc * m.np_c;
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st)));
+      }
+      {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
+        GemmArgs g = gargs((int)HN, m.Ec / 2, m.d2, X, m.d2, bw.ca_wk, m.d2, k, m.Ec);
+        g.bias = bw.ca_bk;
+        g.hd = m.dc;
+        g.tab = tab_ck;
+        g.tab_mod = (int)m.N;
+        g.part = partk;
+        g.ldpart = (long)m.nc * m.np_c;
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st)));
+      }
+      HIP_TRY(finalize(partq, Ht, m.nc, m.np_c, rq));
+      HIP_TRY(finalize(partk, HN, m.nc, m.np_c, rk));
+      {
+        AttnArgs a;
+        a.q = q;
+        a.ldq = m.Ec;
+        a.rq = rq;
+        a.k = k;
+        a.ldk = m.Ec;
+        a.rk = rk;
+        a.xt = XT;
+        a.ldxt = m.Npad;
+        a.opart = (float*)(ws + p.opart);
+        a.mpart = (float*)(ws + p.mpart);
+        a.lpart = (float*)(ws + p.lpart);
+        a.H = m.H;
+        a.N = (int)m.N;
+        a.t = m.t;
+        a.nc = m.nc;
+        a.dc = m.dc;
+        a.d2 = m.d2;
+        const float s = cfg->logit_scale_cross != 0.f ? cfg->logit_scale_cross : (float)m.dc;
+        a.scale_log2 = s * LOG2E;
+        a.keys_per_split = (int)m.keys_per_split;
+        hipError_t e;
+        if (m.d2 == 128) e = launch_attn<CT, 128>(a, m.splits, st);
+        else if (m.d2 == 256) e = launch_attn<CT, 256>(a, m.splits, st);
+        else e = launch_attn<CT, 512>(a, m.splits, st);
+        HIP_TRY(e);
+        hipLaunchKernelGGL((merge_kernel<CT>), dim3((unsigned)(Ht * m.nc)), dim3(256), 0, st, a.opart, a.mpart,
+                           a.lpart, m.splits, m.H, m.nc, m.t, m.d2, O);
+        HIP_TRY(hipGetLastError());
+      }
+      {  // head_c = O_c W_V,c^T   (batched over cross heads c)
+        GemmArgs g = gargs((int)Ht, m.dc, m.d2, O, (long)m.nc * m.d2, bw.ca_wv, m.d2, head, m.Ec);
+        g.nb2 = m.nc;
+        g.sA2 = m.d2;
+        g.sB2 = (long)m.dc * m.d2;
+        g.sC2 = m.dc;
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_STORE>(g, m.nc, st)));
+      }
+      {  // Z += Concat(heads) W_O^T
+        GemmArgs g = gargs((int)Ht, m.D, m.Ec, head, m.Ec, bw.ca_wo, m.Ec, Z, m.D);
+        HIP_TRY((gemm<CT, CT, IT, float, IT, EPI_RESID>(g, 1, st)));
+      }
+    }
+    // ---------------- latent self-attention: Z += SelfAttn(RMSNorm(Z))
+    if (m.ns > 0) {
+      CT* qs = (CT*)(ws + p.qs);
+      CT* ks = (CT*)(ws + p.ks);
+      CT* vT = (CT*)(ws + p.vT);
+      float* partqs = (float*)(ws + p.partqs);
+      float* partks = (float*)(ws + p.partks);
+      float* rqs = (float*)(ws + p.rqs);
+      float* rks = (float*)(ws + p.rks);
+      float* Ssa = (float*)(ws + p.Ssa);
+      CT* Psa = (CT*)(ws + p.Psa);
+      CT* Osa = (CT*)(ws + p.Osa);
+      HIP_TRY(rmsnorm());
+      {
+        GemmArgs g = gargs((int)Ht, m.Es / 2, m.D, Y, m.D, bw.sa_wq, m.D, qs, m.Es);
+        g.bias = bw.sa_bq;
+        g.hd = m.ds;
+        g.part = partqs;
+        g.ldpart = (long)m.ns * m.np_s;
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st)));
+        g.B = bw.sa_wk;
+        g.bias = bw.sa_bk;
+        g.C = ks;
+        g.part = partks;
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st)));
+      }
+      {  // v^T[h] = W_V^sa Y[h]^T : [Es][tpad] per KV head
+        GemmArgs g = gargs(m.Es, m.t, m.D, bw.sa_wv, m.D, Y, m.D, vT, m.tpad);
+        g.sB1 = (long)m.t * m.D;
+        g.sC1 = (long)m.Es * m.tpad;
+        HIP_TRY((gemm<CT, IT, CT, CT, IT, EPI_STORE>(g, m.H, st)));
+        if (m.tpad > m.t) {
+          hipLaunchKernelGGL((zero_cols_kernel<CT>), dim3(grid1d((long)m.H * m.Es * (m.tpad - m.t))), dim3(256), 0,
+                             st, vT, (long)m.H * m.Es, m.tpad, m.t, m.tpad);
+          HIP_TRY(hipGetLastError());
+        }
+      }
+      HIP_TRY(finalize(partqs, Ht, m.ns, m.np_s, rqs));
+      HIP_TRY(finalize(partks, Ht, m.ns, m.np_s, rks));
+      {  // S = s * q k^T with the QK-norm factors, per (h, c)
+        GemmArgs g = gargs(m.t, m.t, m.ds, qs, m.Es, ks, m.Es, Ssa, m.tpad);
+        g.nb2 = m.ns;
+        g.sA1 = (long)m.t * m.Es;
+        g.sA2 = m.ds;
+        g.sB1 = (long)m.t * m.Es;
+        g.sB2 = m.ds;
+        g.sC1 = (long)m.ns * m.t * m.tpad;
+        g.sC2 = (long)m.t * m.tpad;
+        g.scale = cfg->logit_scale_self != 0.f ? cfg->logit_scale_self : (float)m.ds;
+        g.rq = rqs;
+        g.ldrq = m.ns;
+        g.sQ1 = (long)m.t * m.ns;
+        g.sQ2 = 1;
+        g.rk = rks;
+        g.ldrk = m.ns;
+        g.sK1 = (long)m.t * m.ns;
+        g.sK2 = 1;
+        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_SCALE>(g, m.H * m.ns, st)));
+      }
+      hipLaunchKernelGGL((softmax_rows_kernel<CT>), dim3((unsigned)(((long)m.H * m.ns * m.t + 3) / 4)), dim3(256), 0,
+                         st, Ssa, Psa, (long)m.H * m.ns * m.t, m.t, m.tpad);
+      HIP_TRY(hipGetLastError());
+      {  // O = P v per (h, c)
+        GemmArgs g = gargs(m.t, m.ds, m.tpad, Psa, m.tpad, vT, m.tpad, Osa, m.Es);
+        g.nb2 = m.ns;
+        g.sA1 = (long)m.ns * m.t * m.tpad;
+        g.sA2 = (long)m.t * m.tpad;
+        g.sB1 = (long)m.Es * m.tpad;
+        g.sB2 = (long)m.ds * m.tpad;
+        g.sC1 = (long)m.t * m.Es;
+        g.sC2 = m.ds;
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE>(g, m.H * m.ns, st)));
+      }
+      {
+        GemmArgs g = gargs((int)Ht, m.D, m.Es, Osa, m.Es, bw.sa_wo, m.Es, Z, m.D);
+        HIP_TRY((gemm<CT, CT, IT, float, IT, EPI_RESID>(g, 1, st)));
+      }
+    }
+    // ---------------- FFN: Z += FFN(RMSNorm(Z))
+    if (cfg->ffn_kind != STILL_FFN_NONE) {
+      CT* hid = (CT*)(ws + p.hid);
+      HIP_TRY(rmsnorm());
+      if (cfg->ffn_kind == STILL_FFN_SWIGLU) {
+        GemmArgs g = gargs((int)Ht, m.F, m.D, Y, m.D, bw.ffn_wg, m.D, hid, m.F);
+        g.B2 = bw.ffn_wu;
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_SWIGLU>(g, 1, st)));
+      } else {
+        GemmArgs g = gargs((int)Ht, m.F, m.D, Y, m.D, bw.ffn_wu, m.D, hid, m.F);
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_GELU>(g, 1, st)));
+      }
+      GemmArgs g = gargs((int)Ht, m.D, m.F, hid, m.F, bw.ffn_wd, m.F, Z, m.D);
+      HIP_TRY((gemm<CT, CT, IT, float, IT, EPI_RESID>(g, 1, st)));
+    }
+  }
+  // ---------------- output heads: C_k = Z_out W_key^T (re-rotated), C_v = Z_out W_val^T
+  {
+    GemmArgs gk = gargs((int)Ht, m.d / 2, m.D, Z, m.D, w->w_key, m.D, Ckp, m.d);
+    gk.hd = m.d;
+    gk.tab = rerotate ? tab_bq : nullptr;
+    gk.tab_mod = m.t;
+    GemmArgs gv = gargs((int)Ht, m.d, m.D, Z, m.D, w->w_val, m.D, Cvp, m.d);
+    if (cfg->final_norm) {
+      HIP_TRY(rmsnorm());
+      gk.A = Y;
+      gv.A = Y;
+      HIP_TRY((gemm<CT, CT, IT, IT, IT, EPI_PAIR>(gk, 1, st)));
+      HIP_TRY((gemm<CT, CT, IT, IT, IT, EPI_STORE>(gv, 1, st)));
+    } else {
+      HIP_TRY((gemm<CT, float, IT, IT, IT, EPI_PAIR>(gk, 1, st)));
+      HIP_TRY((gemm<CT, float, IT, IT, IT, EPI_STORE>(gv, 1, st)));
+    }
+  }
+  return STILL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Validation of a layer's pointers
+// ---------------------------------------------------------------------------
+static bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
+
+static still_status check_ptr(const void* p, const char* name, bool required) {
+  if (!p) return required ? fail(STILL_E_INVAL, "%s is NULL", name) : STILL_OK;
+  if (misaligned(p)) return fail(STILL_E_INVAL, "%s is not 16-byte aligned", name);
+  return STILL_OK;
+}
+
+static still_status check_layer(const still_config* c, const Dims& m, const still_layer_weights* w, int layer) {
+  if (!w) return fail(STILL_E_INVAL, "layer %d: weights NULL", layer);
+  if (w->t_bank != m.t) return fail(STILL_E_SHAPE, "layer %d: t=%d but latent bank holds %d", layer, m.t, w->t_bank);
+  still_status s;
+#define CHK(p, req)                                                        \
+  if ((s = check_ptr((p), #p, (req))) != STILL_OK) {                       \
+    g_last_error = "layer " + std::to_string(layer) + ": " + g_last_error; \
+    return s;                                                              \
+  }
+  CHK(w->latents, true);
+  CHK(w->w_key, true);
+  CHK(w->w_val, true);
+  if (!w->blocks) return fail(STILL_E_INVAL, "layer %d: blocks NULL", layer);
+  for (int b = 0; b < c->n_blocks; ++b) {
+    const still_block_weights& bw = w->blocks[b];
+    const bool ca = c->cross_every_block || b == 0;
+    CHK(bw.ca_wq, ca);
+    CHK(bw.ca_bq, false);
+    CHK(bw.ca_wk, ca);
+    CHK(bw.ca_bk, false);
+    CHK(bw.ca_wv, ca);
+    CHK(bw.ca_wo, ca);
+    const bool sa = m.ns > 0;
+    CHK(bw.sa_wq, sa);
+    CHK(bw.sa_bq, false);
+    CHK(bw.sa_wk, sa);
+    CHK(bw.sa_bk, false);
+    CHK(bw.sa_wv, sa);
+    CHK(bw.sa_wo, sa);
+    CHK(bw.ffn_wg, c->ffn_kind == STILL_FFN_SWIGLU);
+    CHK(bw.ffn_wu, c->ffn_kind != STILL_FFN_NONE);
+    CHK(bw.ffn_wd, c->ffn_kind != STILL_FFN_NONE);
+  }
+#undef CHK
+  return STILL_OK;
+}
+
+static still_status compact(const still_config* cfg, int32_t L, const still_layer_weights* w, const void* const* K,
+                            const void* const* V, const double* positions, int64_t N, double rope_theta, int32_t t,
+                            uint32_t flags, void* const* Ck, void* const* Cv, double* out_positions, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  Dims m;
+  still_status s = make_dims(cfg, N, t, &m);
+  if (s != STILL_OK) return s;
+  if (L < 1) return fail(STILL_E_INVAL, "n_layers must be >= 1");
+  if (!w || !K || !V || !Ck || !Cv) return fail(STILL_E_INVAL, "NULL layer array");
+  if (flags & ~(uint32_t)STILL_F_REROTATE) return fail(STILL_E_INVAL, "unknown flags 0x%x", flags);
+  if (!(rope_theta > 0.0)) return fail(STILL_E_INVAL, "rope_theta must be > 0");
+  if (!positions) return fail(STILL_E_INVAL, "positions is NULL");
+  if (((uintptr_t)positions & 7u) || ((uintptr_t)out_positions & 7u))
+    return fail(STILL_E_INVAL, "positions / out_positions must be 8-byte aligned");
+  for (int l = 0; l < L; ++l) {
+    if ((s = check_layer(cfg, m, &w[l], l)) != STILL_OK) return s;
+    if (!K[l] || !V[l] || !Ck[l] || !Cv[l]) return fail(STILL_E_INVAL, "layer %d: NULL cache or output pointer", l);
+    if (misaligned(K[l]) || misaligned(V[l]) || misaligned(Ck[l]) || misaligned(Cv[l]))
+      return fail(STILL_E_INVAL, "layer %d: cache/output pointers must be 16-byte aligned", l);
+  }
+  const Plan p = make_plan(m);
+  if (!workspace) return fail(STILL_E_WORKSPACE, "workspace is NULL");
+  if (workspace_bytes < p.total)
+    return fail(STILL_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, p.total);
+  char* ws = (char*)(((uintptr_t)workspace + 255) & ~(uintptr_t)255);
+  hipStream_t st = (hipStream_t)stream;
+  (void)hipGetLastError();  // clear a stale error so launch checks report this call
+  const bool rerot = (flags & STILL_F_REROTATE) != 0;
+  if ((s = prepare_tables(m, p, ws, positions, rope_theta, cfg->compactor_rope_base, rerot, out_positions, st)) !=
+      STILL_OK)
+    return s;
+  for (int l = 0; l < L; ++l) {
+    s = m.fp32 ? run_layer<float, float>(cfg, m, p, ws, &w[l], K[l], V[l], rerot, Ck[l], Cv[l], st)
+               : run_layer<bf16, f16>(cfg, m, p, ws, &w[l], K[l], V[l], rerot, Ck[l], Cv[l], st);
+    if (s != STILL_OK) return s;
+  }
+  return STILL_OK;
+}
+
+}  // namespace still
+
+using namespace still;
+
+extern "C" {
+
+size_t still_workspace_size(const still_config* cfg, int64_t N, int32_t t, int32_t n_layers) {
+  Dims m;
+  if (n_layers < 1 || make_dims(cfg, N, t, &m) != STILL_OK) return 0;
+  return make_plan(m).total;
+}
+
+still_status still_compact_layer(const still_config* cfg, const still_layer_weights* w, const void* K, const void* V,
+                                 const double* positions, int64_t N, double rope_theta, int32_t t, uint32_t flags,
+                                 void* C_k, void* C_v, double* out_positions, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  const void* Ka[1] = {K};
+  const void* Va[1] = {V};
+  void* Cka[1] = {C_k};
+  void* Cva[1] = {C_v};
+  return compact(cfg, 1, w, Ka, Va, positions, N, rope_theta, t, flags, Cka, Cva, out_positions, workspace,
+                 workspace_bytes, stream);
+}
+
+still_status still_compact_model(const still_config* cfg, int32_t n_layers, const still_layer_weights* w,
+                                 const void* const* K, const void* const* V, const double* positions, int64_t N,
+                                 double rope_theta, int32_t t, uint32_t flags, void* const* C_k, void* const* C_v,
+                                 double* out_positions, void* workspace, size_t workspace_bytes, void* stream) {
+  return compact(cfg, n_layers, w, K, V, positions, N, rope_theta, t, flags, C_k, C_v, out_positions, workspace,
+                 workspace_bytes, stream);
+}
+
+const char* still_status_string(int32_t s) {
+  switch (s) {
+    case STILL_OK: return "STILL_OK";
+    case STILL_E_INVAL: return "STILL_E_INVAL";
+    case STILL_E_SHAPE: return "STILL_E_SHAPE";
+    case STILL_E_DTYPE: return "STILL_E_DTYPE";
+    case STILL_E_WORKSPACE: return "STILL_E_WORKSPACE";
+    case STILL_E_UNSUPPORTED: return "STILL_E_UNSUPPORTED";
+    case STILL_E_HIP: return "STILL_E_HIP";
+    default: return "STILL_E_UNKNOWN";
+  }
+}
+
+const char* still_last_error(void) { return g_last_error.c_str(); }
+
+const char* still_version(void) { return "still-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+"""C-ABI contract checks that need no GPU: the library loads, exports every
+function include/still.h declares, and rejects invalid arguments with the
+documented status codes before enqueuing any work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_07878_amd import binding, configs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "still.h")
+
+FAKE = 0x10000   # never dereferenced: validation fails before any device access
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(still_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"still_compact_layer", "still_compact_model", "still_workspace_size"} <= set(names)
+    lib = binding.lib()
+    for n in names:
+        assert hasattr(lib, n), f"{n} not exported"
+
+
+def test_status_strings_and_version():
+    for code, name in binding.STATUS.items():
+        assert binding.still_status_string(code) == name
+    assert "gfx950" in binding.still_version()
+
+
+def _cfg(**kw):
+    base = configs.get_workload(1).cfg
+    c = binding.make_config(base)
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+class FakeWeights:
+    """still_layer_weights with fake (aligned, never dereferenced) device pointers."""
+
+    def __init__(self, cfg, t_bank, drop=None, misalign=None):
+        self.blocks = (binding.still_block_weights * cfg.n_blocks)()
+        for b in range(cfg.n_blocks):
+            for f, _ in binding.still_block_weights._fields_:
+                setattr(self.blocks[b], f, FAKE)
+        if drop:
+            setattr(self.blocks[0], drop, None)
+        if misalign:
+            setattr(self.blocks[0], misalign, FAKE + 2)
+        self.struct = binding.still_layer_weights(FAKE, t_bank, self.blocks, FAKE, FAKE)
+
+
+def call(cfg, w, N=2048, t=256, K=FAKE, ws_bytes=1 << 40, flags=1, positions=FAKE, ws=FAKE):
+    return binding.lib().still_compact_layer(ctypes.byref(cfg), ctypes.byref(w.struct), K, FAKE, positions, N,
+                                             1e6, t, flags, FAKE, FAKE, None, ws, ws_bytes, None)
+
+
+def test_workspace_size():
+    c = _cfg()
+    n = binding.still_workspace_size(c, 2048, 256, 1)
+    assert n > 0
+    assert binding.still_workspace_size(c, 4096, 256, 1) > n
+    assert binding.still_workspace_size(_cfg(head_dim=96), 2048, 256, 1) == 0
+    assert binding.still_workspace_size(c, 0, 256, 1) == 0
+    assert binding.still_workspace_size(c, 2048, 256, 0) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(mode=7), -3),
+    (dict(head_dim=63), -2),
+    (dict(head_dim=96), -5),
+    (dict(n_kv_heads=0), -1),
+    (dict(n_cross_heads=0), -1),
+    (dict(ffn_kind=9), -1),
+    (dict(cross_head_dim=96), -5),
+    (dict(compactor_rope_base=0.0), -1),
+])
+def test_bad_config(kw, status):
+    c = _cfg(**kw)
+    assert call(c, FakeWeights(c, 256)) == status
+    assert binding.still_last_error()
+
+
+def test_bank_size_mismatch():
+    c = _cfg()
+    assert call(c, FakeWeights(c, 128)) == -2
+    assert "latent bank" in binding.still_last_error()
+
+
+def test_null_and_misaligned_pointers():
+    c = _cfg()
+    assert call(c, FakeWeights(c, 256), K=None) == -1
+    assert call(c, FakeWeights(c, 256), positions=None) == -1
+    assert call(c, FakeWeights(c, 256, drop="ca_wq")) == -1
+    assert call(c, FakeWeights(c, 256, misalign="sa_wo")) == -1
+    assert call(c, FakeWeights(c, 256), K=FAKE + 4) == -1
+    # a NULL bias is allowed (zero bias): fails only later, at the workspace check
+    assert call(c, FakeWeights(c, 256, drop="ca_bq"), ws_bytes=16) == -4
+
+
+def test_bad_sizes_and_flags():
+    c = _cfg()
+    assert call(c, FakeWeights(c, 256), N=0) == -1
+    assert call(c, FakeWeights(c, 0), t=0) == -1
+    assert call(c, FakeWeights(c, 256), flags=0x8) == -1
+
+
+def test_workspace_checks():
+    c = _cfg()
+    need = binding.still_workspace_size(c, 2048, 256, 1)
+    assert call(c, FakeWeights(c, 256), ws_bytes=need - 1) == -4
+    assert call(c, FakeWeights(c, 256), ws=None) == -4
+
+
+def test_model_entry_validates_every_layer():
+    c = _cfg()
+    ws = [FakeWeights(c, 256), FakeWeights(c, 128)]
+    arr = (binding.still_layer_weights * 2)(*[w.struct for w in ws])
+    ptrs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    r = binding.lib().still_compact_model(ctypes.byref(c), 2, arr, ptrs, ptrs, FAKE, 2048, 1e6, 256, 1,
+                                          ptrs, ptrs, None, FAKE, 1 << 40, None)
+    assert r == -2
+    assert "layer 1" in binding.still_last_error()
