@@ -1,0 +1,186 @@
+#!/usr/bin/env python3
+"""Benchmark: cache tokens compacted per second per layer on one MI355X.
+
+One step = one still_compact_model call over every layer of the workload (the
+whole hot path: RoPE-fix staging, cross-attention, self-attention, FFN, output
+heads, re-rotation) with inputs already resident in HBM.  Prints one JSON line.
+
+The dominant kernel (flash cross-attention) is timed live with hipEvent pairs
+on its launch stream during the timed region; its algorithmic FLOPs per launch
+(QK^T and P.X for all KV heads x cross heads of one layer) divided by the
+average launch duration gives the roofline point.  The fp64 oracle is timed
+on a bounded sample (one KV head of one layer) as a CPU baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP16_TFLOPS = 2500.0     # MI355X dense fp16/bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def ca_flops_per_launch(w) -> float:
+    c = w.cfg
+    per_pair = 2.0 * w.t * w.n_tokens * (c.dc + 2 * c.head_dim)
+    return per_pair * c.n_kv_heads * c.n_cross_heads
+
+
+def layer_flops(w, N=None) -> float:
+    """Algorithmic FLOPs of one layer (cheapest exact association)."""
+    c = w.cfg
+    N = N or w.n_tokens
+    H, t, D, d, nc, dc, ns, ds, F = (c.n_kv_heads, w.t, c.latent_dim, c.head_dim, c.n_cross_heads, c.dc,
+                                     c.n_self_heads, c.ds, c.ffn_hidden)
+    Ht = H * t
+    f = 2.0 * Ht * D * nc * dc                          # Q projection
+    f += 2.0 * H * N * 2 * d * nc * dc                  # K projection
+    f += 2.0 * H * nc * t * N * (dc + 2 * d)            # QK^T and P.X
+    f += 2.0 * Ht * 2 * d * nc * dc                     # (P X) W_V
+    f += 2.0 * Ht * nc * dc * D                         # W_O
+    if ns:
+        f += 2.0 * Ht * D * 3 * ns * ds + 2.0 * H * ns * t * t * 2 * ds + 2.0 * Ht * ns * ds * D
+    if c.ffn_kind == 1:
+        f += 2.0 * Ht * D * 3 * F
+    elif c.ffn_kind == 2:
+        f += 2.0 * Ht * D * 2 * F
+    f += 2.0 * Ht * D * 2 * d                           # output heads
+    return f
+
+
+def cpu_baseline(w, budget_s: float = 30.0) -> dict:
+    """Time the fp64 oracle on one KV head of layer 0 (numpy, all BLAS threads)."""
+    import numpy as np
+    from oracle import compactor
+    from paper_2606_07878_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 0) for i in threadpool_info() if i.get("user_api") == "blas"] or [0])
+    except Exception:
+        threads = 0
+    cache = synth.as_f64(synth.make_cache(w, 0))
+    wts = synth.as_f64(synth.make_weights(w, 0))
+    t0 = time.perf_counter()
+    compactor.compact_layer(cache["K"], cache["V"], cache["positions"], w.rope_theta, wts, w.cfg, w.t,
+                            heads=[0])
+    dt = time.perf_counter() - t0
+    per_layer = dt * w.cfg.n_kv_heads
+    return {"value": w.n_tokens / per_layer, "unit": "tokens/s/layer", "cores": int(threads or os.cpu_count()),
+            "kind": "oracle",
+            "sample": f"fp64 oracle, layer 0, KV head 0 of {w.cfg.n_kv_heads} ({dt:.1f} s), "
+                      f"scaled x{w.cfg.n_kv_heads} to one layer"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=2, help="registered workload id (default: 8k/8x Qwen-8B stack)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the compactor forward runs on a "
+              "single MI355X in this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_07878_amd import binding, configs, synth
+
+    w = configs.get_workload(args.workload)
+    if w.rounds:
+        raise SystemExit("iterative workloads are benchmarked by their parity tests, not bench.py")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L = w.n_layers
+    print(f"[bench] generating {L} layers of {w.name}", file=sys.stderr, flush=True)
+    Ks, Vs, Ws = [], [], []
+    pos = None
+    for l in range(L):
+        K, V, pos, W = synth.make_layer_torch(w, l, dev)
+        Ks.append(K)
+        Vs.append(V)
+        Ws.append(binding.LayerWeights(w.cfg, W))
+    ccfg = binding.make_config(w.cfg, configs.MODE_BF16)
+    N, t = w.n_tokens, w.t
+    ws_bytes = binding.still_workspace_size(ccfg, N, t, L)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    Ck = [torch.empty(w.cfg.n_kv_heads, t, w.cfg.head_dim, dtype=torch.bfloat16, device=dev) for _ in range(L)]
+    Cv = [torch.empty_like(c) for c in Ck]
+    outp = torch.empty(t, dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        st = binding.still_compact_model(ccfg, Ws, Ks, Vs, pos, N, w.rope_theta, t, binding.STILL_F_REROTATE,
+                                         Ck, Cv, outp, ws, ws_bytes, stream.cuda_stream)
+        if st != 0:
+            raise binding.StillError(st, binding.still_last_error())
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    binding.still_timing_reset()
+    binding.still_timing_enable(1 << binding.KERNEL_CLASSES["cross_attn"])
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    binding.still_timing_enable(0)
+    ms_step = e0.elapsed_time(e1) / args.steps
+    att_ms, att_n = binding.still_timing_read(binding.KERNEL_CLASSES["cross_attn"])
+    print(f"[bench] {args.steps} steps, {ms_step:.2f} ms/step", file=sys.stderr, flush=True)
+
+    # per-class breakdown (separate, untimed pass)
+    binding.still_timing_reset()
+    binding.still_timing_enable((1 << 6) - 1)
+    step()
+    torch.cuda.synchronize()
+    binding.still_timing_enable(0)
+    breakdown = {}
+    for name, cls in binding.KERNEL_CLASSES.items():
+        ms, n = binding.still_timing_read(cls)
+        if n:
+            breakdown[name] = round(ms / L, 4)
+    binding.still_timing_reset()
+
+    tokens_per_s_layer = N * L / (ms_step / 1e3)
+    avg_att_s = att_ms / att_n / 1e3
+    achieved = ca_flops_per_launch(w) / avg_att_s / 1e12
+    out = {
+        "metric": "cache tokens compacted/sec/layer + % HBM BW or % MFMA peak, 1 MI355X",
+        "value": round(tokens_per_s_layer, 1),
+        "unit": "tokens/s/layer",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic",
+        "config": {"workload": w.name, "layers": L, "N": N, "t": t, "H_kv": w.cfg.n_kv_heads,
+                   "d": w.cfg.head_dim, "D": w.cfg.latent_dim, "n_cross": w.cfg.n_cross_heads,
+                   "n_self": w.cfg.n_self_heads, "ffn_hidden": w.cfg.ffn_hidden, "io": "bf16",
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "mfma", "kernel": "cross_attn", "achieved": round(achieved, 2),
+                     "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP16_TFLOPS, 4),
+                     "traffic": None, "avg_launch_ms": round(avg_att_s * 1e3, 4), "launches": att_n,
+                     "flops_per_launch": ca_flops_per_launch(w)},
+        "layer_mfma_frac": round(layer_flops(w) / (ms_step / L / 1e3) / 1e12 / PEAK_FP16_TFLOPS, 4),
+        "kernel_ms_per_layer": breakdown,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

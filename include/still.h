@@ -153,6 +153,27 @@ const char *still_status_string(int32_t status);
 /* Detail of the last non-OK status returned on the calling thread. */
 const char *still_last_error(void);
 
+/* Optional event timing of the library's kernels, for benchmarks.
+ * still_timing_enable(mask) makes every subsequent launch of a kernel class c
+ * with bit (1 << c) set in mask record a hipEvent pair on its launch stream;
+ * still_timing_enable(0) stops recording.  still_timing_read waits for the recorded events, returns
+ * the summed duration (ms) and launch count of one class since the last
+ * still_timing_reset, and may be called while the stream is idle only.
+ * Event objects are created on first use and reused; nothing else is
+ * allocated.  Not thread-safe: time one stream from one thread. */
+enum {
+  STILL_K_CROSS_ATTN = 0,   /* flash latent->cache cross-attention            */
+  STILL_K_KPROJ = 1,        /* cross-attention key projection (+RoPE, norms)  */
+  STILL_K_QPROJ = 2,        /* cross-attention query projection               */
+  STILL_K_REFINE = 3,       /* exact-logit refinement of the top keys         */
+  STILL_K_LATENT = 4,       /* latent-side GEMMs (V/O proj, self-attn, FFN, heads) */
+  STILL_K_OTHER = 5,        /* staging, norms, softmax, merge, tables          */
+  STILL_K_COUNT = 6
+};
+still_status still_timing_enable(int32_t class_mask);
+still_status still_timing_reset(void);
+still_status still_timing_read(int32_t kernel_class, double *total_ms, int64_t *launches);
+
 /* Library version string. */
 const char *still_version(void);
 

@@ -87,6 +87,13 @@ def lib():
         L.still_last_error.restype = ctypes.c_char_p
         L.still_version.argtypes = []
         L.still_version.restype = ctypes.c_char_p
+        L.still_timing_enable.argtypes = [ctypes.c_int32]
+        L.still_timing_enable.restype = ctypes.c_int32
+        L.still_timing_reset.argtypes = []
+        L.still_timing_reset.restype = ctypes.c_int32
+        L.still_timing_read.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int64)]
+        L.still_timing_read.restype = ctypes.c_int32
         _lib = L
     return _lib
 
@@ -159,6 +166,27 @@ def still_last_error() -> str:
 
 def still_version() -> str:
     return lib().still_version().decode()
+
+
+# kernel classes of the timing facility (still.h)
+KERNEL_CLASSES = {"cross_attn": 0, "kproj": 1, "qproj": 2, "refine": 3, "latent": 4, "other": 5}
+
+
+def still_timing_enable(class_mask: int) -> None:
+    """Record hipEvent pairs around launches of the classes in class_mask (0 = off)."""
+    _check(lib().still_timing_enable(int(class_mask)))
+
+
+def still_timing_reset() -> None:
+    _check(lib().still_timing_reset())
+
+
+def still_timing_read(kernel_class: int):
+    """(total ms, launches) of one kernel class since the last reset."""
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(lib().still_timing_read(kernel_class, ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 # ----------------------------------------------------------------------------

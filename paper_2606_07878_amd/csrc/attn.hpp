@@ -35,9 +35,11 @@ struct AttnArgs {
   int H, N, t, nc, dc, d2;
   float scale_log2;  // logit scale * log2(e)
   int keys_per_split;
+  float* cval;       // TOPK > 0: [S][H*nc][t][2*TOPK] largest logits seen (log2 units) ...
+  int* cidx;         // ... and their key indices (-1 = none), per half-lane
 };
 
-template <class CT, int TT, int NB, int DK, int D2>
+template <class CT, int TT, int NB, int DK, int D2, int TOPK>
 __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
   typedef Mma<CT> MM;
   typedef typename MM::frag frag;
@@ -79,6 +81,14 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int f = 0; f < FT; ++f) o[f] = zero16();
   float m_run = -INFINITY, l_run = 0.f;
+  // top-TOPK keys of this lane's half of the key range, by logit (descending)
+  float tv[TOPK > 0 ? TOPK : 1];
+  int ti[TOPK > 0 ? TOPK : 1];
+#pragma unroll
+  for (int q = 0; q < (TOPK > 0 ? TOPK : 1); ++q) {
+    tv[q] = -INFINITY;
+    ti[q] = -1;
+  }
 
   frag rq_[QV], rk_[KVv], rx[XV];
   auto load_qk = [&](int n0, int d0) {
@@ -163,6 +173,22 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
         x = (n0 + kl < nend) ? x : -INFINITY;
         s[kt][j] = x;
         mx = fmaxf(mx, x);
+        if constexpr (TOPK > 0) {
+          if (x > tv[TOPK - 1]) {
+            float v = x;
+            int id = n0 + kl;
+#pragma unroll
+            for (int q = 0; q < TOPK; ++q) {
+              const bool gt = v > tv[q];
+              const float tvq = tv[q];
+              const int tiq = ti[q];
+              tv[q] = gt ? v : tvq;
+              ti[q] = gt ? id : tiq;
+              v = gt ? tvq : v;
+              id = gt ? tiq : id;
+            }
+          }
+        }
       }
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m_run, mx);
@@ -233,6 +259,13 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
     if (lg == 0) {
       a.mpart[row] = m_run;
       a.lpart[row] = l_run;
+    }
+    if constexpr (TOPK > 0) {
+#pragma unroll
+      for (int q = 0; q < TOPK; ++q) {
+        a.cval[row * (2 * TOPK) + lg * TOPK + q] = tv[q];
+        a.cidx[row * (2 * TOPK) + lg * TOPK + q] = ti[q];
+      }
     }
   }
 }

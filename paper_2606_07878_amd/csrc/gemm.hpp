@@ -21,24 +21,38 @@
 
 namespace still {
 
-enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_PAIR = 2, EPI_SWIGLU = 3, EPI_SCALE = 4, EPI_GELU = 5 };
+enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_PAIR = 2, EPI_SWIGLU = 3, EPI_SCALE = 4, EPI_GELU = 5, EPI_REFINE = 6 };
 
 struct GemmArgs {
   int M, N, K;   // N = output columns, or column pairs for PAIR / SWIGLU
   int nb2;       // batch index z -> (z / nb2, z % nb2), strides s*1, s*2 (elements)
   const void* A;
+  const void* A2;      // optional low part of a split A operand: C = (A + A2) B^T, same layout as A
   long lda, sA1, sA2;
   const void* B;
   const void* B2;  // SWIGLU: W_u
   long ldb, sB1, sB2;
+  int bwrap;           // B column k >= bwrap reads column k - bwrap (0 = off)
   void* C;
   long ldc, sC1, sC2;
   const void* bias;    // per output column, NULL = none
+  long sBias2;         // bias offset per unit of the inner batch index
   int hd;              // PAIR: head width
   const float2* tab;   // PAIR: rotation table, row (r % tab_mod), entry [row*hd/2 + j]; NULL = none
   int tab_mod;
   float* part;         // PAIR: per-row sum-of-squares partials, NULL = none
   long ldpart;
+  float* C2;           // PAIR: optional fp32 copy of the (rotated) outputs, ldc as C
+  // REFINE: row r of batch (b1, b2) is candidate slot r of latent i = r / R;
+  // its key index is ridx[r] (< 0: empty).  The epilogue rotates by tab[key],
+  // dots with qex row i and writes (dot, sum of squares) partials.
+  const int* ridx;
+  long sI1, sI2;
+  int R;
+  const float* qex;
+  long ldqex, sE1, sE2;
+  float2* rpart;
+  long sR1, sR2;
   float scale;         // SCALE: C = acc * scale * rq[r] * rk[col]
   const float* rq;
   long ldrq, sQ1, sQ2;
@@ -59,7 +73,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int TM = BM / 64, TN = BN / 64;    // 32x32 tiles per wave
   constexpr int KV = BK / E;                   // 16-byte vectors per tile row
   constexpr int AV = BM * KV / 256, BV = BN * KV / 256;
-  constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU);
+  constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
   static_assert(AV >= 1 && BV >= 1 && BM * KV % 256 == 0 && BN * KV % 256 == 0, "tile/threads");
   static_assert(TN % 2 == 0, "BN must allow two column halves per wave");
 
@@ -97,7 +111,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       const int half = lc / (BN / 2);
       const int P = nt * (BN / 2) + (lc % (BN / 2));
       bvalid[i] = P < N;
-      if (EPI == EPI_PAIR) {
+      if (EPI == EPI_PAIR || EPI == EPI_REFINE) {
         const int c = P / hh, j = P - c * hh;
         brow_ptr[i] = B + (long)(c * g.hd + j + half * hh) * g.ldb;
       } else {
@@ -110,18 +124,20 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     }
   }
 
-  auto load_stage = [&](int k0) {
+  const TA* Alo = g.A2 ? (const TA*)g.A2 + b1 * g.sA1 + b2 * g.sA2 : nullptr;
+  auto load_stage = [&](int k0, const TA* Ap) {
 #pragma unroll
     for (int i = 0; i < AV; ++i) {
       const int v = tid + i * 256, r = v / KV, kk = (v % KV) * E;
       const int gr = m0 + r, gk = k0 + kk;
-      ra[i] = (gr < M && gk < K) ? VecLoad<CT, TA>::load(A + (long)gr * g.lda + gk) : zero_frag<CT>();
+      ra[i] = (gr < M && gk < K) ? VecLoad<CT, TA>::load(Ap + (long)gr * g.lda + gk) : zero_frag<CT>();
     }
 #pragma unroll
     for (int i = 0; i < BV; ++i) {
       const int v = tid + i * 256, kk = (v % KV) * E;
       const int gk = k0 + kk;
-      rb[i] = (bvalid[i] && gk < K) ? VecLoad<CT, TB>::load(brow_ptr[i] + gk) : zero_frag<CT>();
+      const int gkb = (g.bwrap && gk >= g.bwrap) ? gk - g.bwrap : gk;
+      rb[i] = (bvalid[i] && gk < K) ? VecLoad<CT, TB>::load(brow_ptr[i] + gkb) : zero_frag<CT>();
     }
   };
   auto store_stage = [&](int buf) {
@@ -149,13 +165,18 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int b = 0; b < TN; ++b) acc[a][b] = zero16();
 
-  const int nk = (K + BK - 1) / BK;
-  load_stage(0);
+  const int nk1 = (K + BK - 1) / BK;
+  const int nk = Alo ? 2 * nk1 : nk1;      // split A: second pass over K with the low part
+  load_stage(0, A);
   store_stage(0);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) load_stage((kt + 1) * BK);
+    if (kt + 1 < nk) {
+      const int kn = kt + 1;
+      if (kn < nk1) load_stage(kn * BK, A);
+      else load_stage((kn - nk1) * BK, Alo);
+    }
 #pragma unroll
     for (int ks = 0; ks < BK / (2 * E); ++ks) {
       frag af[TM], bfr[TN];
@@ -176,7 +197,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 
   // ------------------------------------------------------------------ epilogue
   TC* C = (TC*)g.C + b1 * g.sC1 + b2 * g.sC2;
-  const TBias* bias = (const TBias*)g.bias;
+  const TBias* bias = g.bias ? (const TBias*)g.bias + b2 * g.sBias2 : nullptr;
   if constexpr (!PAIRED) {
 #pragma unroll
     for (int a = 0; a < TM; ++a)
@@ -205,11 +226,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
         }
       }
   } else {
-    float ss[TM][16];
+    float ss[TM][16], dd[TM][16];
 #pragma unroll
     for (int a = 0; a < TM; ++a)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) ss[a][j] = 0.f;
+      for (int j = 0; j < 16; ++j) ss[a][j] = dd[a][j] = 0.f;
 #pragma unroll
     for (int b = 0; b < TN / 2; ++b) {
       const int P = nt * (BN / 2) + wn * (BN / 4) + b * 32 + l32;
@@ -226,6 +247,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       } else {
         const int c = P / hh, jp = P - c * hh;
         const int col0 = c * g.hd + jp, col1 = col0 + hh;
+        const int* ridx = (EPI == EPI_REFINE) ? g.ridx + b1 * g.sI1 + b2 * g.sI2 : nullptr;
         const float bv0 = bias ? to_f32(bias[col0]) : 0.f;
         const float bv1 = bias ? to_f32(bias[col1]) : 0.f;
 #pragma unroll
@@ -238,14 +260,50 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
             ss[a][j] += v0 * v0 + v1 * v1;
             float y0 = v0, y1 = v1;
             if (g.tab) {
-              const float2 cs = g.tab[(long)(r % g.tab_mod) * hh + jp];
+              long trow;
+              if constexpr (EPI == EPI_REFINE) {
+                const int key = ridx[r];
+                trow = key < 0 ? 0 : key;
+              } else {
+                trow = r % g.tab_mod;
+              }
+              const float2 cs = g.tab[trow * hh + jp];
               y0 = v0 * cs.x - v1 * cs.y;
               y1 = v1 * cs.x + v0 * cs.y;
             }
-            C[(long)r * g.ldc + col0] = from_f32<TC>(y0);
-            C[(long)r * g.ldc + col1] = from_f32<TC>(y1);
+            if constexpr (EPI == EPI_REFINE) {
+              const int i = r / g.R;
+              const float* qe = g.qex + b1 * g.sE1 + b2 * g.sE2 + (long)i * g.ldqex;
+              dd[a][j] += y0 * qe[col0] + y1 * qe[col1];
+            } else {
+              C[(long)r * g.ldc + col0] = from_f32<TC>(y0);
+              C[(long)r * g.ldc + col1] = from_f32<TC>(y1);
+              if (g.C2) {
+                g.C2[(long)r * g.ldc + col0] = y0;
+                g.C2[(long)r * g.ldc + col1] = y1;
+              }
+            }
           }
       }
+    }
+    if constexpr (EPI == EPI_REFINE) {
+      const int P0 = nt * (BN / 2);
+      const int nparts = (hh / (BN / 2)) * 2;
+      const int pidx = (P0 / (BN / 2)) * 2 + wn;
+      float2* rp = g.rpart + b1 * g.sR1 + b2 * g.sR2;
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          float s = ss[a][j], q = dd[a][j];
+#pragma unroll
+          for (int o = 1; o < 32; o <<= 1) {
+            s += __shfl_xor(s, o);
+            q += __shfl_xor(q, o);
+          }
+          const int r = m0 + wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3);
+          if (l32 == 0 && r < M) rp[(long)r * nparts + pidx] = make_float2(q, s);
+        }
     }
     if constexpr (EPI == EPI_PAIR) {
       if (g.part) {
@@ -274,7 +332,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 
 template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK>
 hipError_t launch_gemm(const GemmArgs& g, int batch, hipStream_t st) {
-  constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU);
+  constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
   const int ntn = PAIRED ? (g.N + BN / 2 - 1) / (BN / 2) : (g.N + BN - 1) / BN;
   const int ntm = (g.M + BM - 1) / BM;
   if (ntn <= 0 || ntm <= 0 || batch <= 0) return hipSuccess;

@@ -126,6 +126,28 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
   for (int i = lane; i < D; i += 64) Y[row * D + i] = from_f32<OT>(z[i] * r);
 }
 
+// Y = RMSNorm(Z) split into a high and a low fp16 part (Y ~= hi + lo to
+// about 22 bits) for products whose result must be more accurate than one
+// fp16 rounding of Y allows.
+__global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float* __restrict__ Z, f16* __restrict__ Yhi,
+                                                            f16* __restrict__ Ylo, long rows, int D, float eps) {
+  const long row = blockIdx.x * 4L + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* z = Z + row * D;
+  float s = 0.f;
+  for (int i = lane; i < D; i += 64) s += z[i] * z[i];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  const float r = 1.f / sqrtf(s / (float)D + eps);
+  for (int i = lane; i < D; i += 64) {
+    const float y = z[i] * r;
+    const f16 hi = (f16)y;
+    Yhi[row * D + i] = hi;
+    Ylo[row * D + i] = (f16)(y - (float)hi);
+  }
+}
+
 // rn[r][c] = 1 / max(sqrt(sum_p part[r][c][p]), eps)   (QK-norm factors)
 __global__ void finalize_norm_kernel(const float* __restrict__ part, long rows, int nh, int np,
                                      float eps, float* __restrict__ rn) {
@@ -140,9 +162,22 @@ __global__ void finalize_norm_kernel(const float* __restrict__ part, long rows, 
 
 // Row softmax of the self-attention logits: S [rows][ld] fp32 (first t
 // columns valid) -> P (columns >= t set to zero).  One wave per row.
+// With `ref` (fp32 mode), the row's 4 largest logits are first recomputed from
+// the fp32 q and k rows with a tree-reduced dot product: the MFMA product
+// accumulates the head width sequentially, and the d_l logit scale amplifies
+// that rounding for exactly the keys that carry the row's mass.
+struct SoftmaxRefine {
+  const float* q;     // [H*t][Es]  un-normalised self-attention queries (fp32)
+  const float* k;     // [H*t][Es]  keys
+  const float* rq;    // [H*t][ns]  1 / ||q~||
+  const float* rk;    // [H*t][ns]
+  int Es, ds, ns, t;
+  float scale;
+};
+
 template <class CT>
 __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* __restrict__ S, CT* __restrict__ P,
-                                                           long rows, int t, int ld) {
+                                                           long rows, int t, int ld, SoftmaxRefine ref) {
   const long row = blockIdx.x * 4L + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
@@ -151,19 +186,174 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* __restri
   for (int i = lane; i < t; i += 64) m = fmaxf(m, s[i]);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  int fix_j[4];
+  float fix_v[4];
+  int nfix = 0;
+  if (ref.q) {
+    // pick the row's 4 largest logits one at a time (ties: lowest column)
+    float last = INFINITY;
+    int lastj = -1;
+    for (int r = 0; r < 4; ++r) {
+      float bv = -INFINITY;
+      int bj = 0x7fffffff;
+      for (int i = lane; i < t; i += 64) {
+        const float v = s[i];
+        const bool after = v < last || (v == last && i > lastj);
+        if (after && (v > bv || (v == bv && i < bj))) {
+          bv = v;
+          bj = i;
+        }
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(bv, o);
+        const int oj = __shfl_xor(bj, o);
+        if (ov > bv || (ov == bv && oj < bj)) {
+          bv = ov;
+          bj = oj;
+        }
+      }
+      if (bj >= t) break;
+      last = bv;
+      lastj = bj;
+      const long hc = row / t;
+      const int i = (int)(row - hc * t);
+      const int h = (int)(hc / ref.ns), c = (int)(hc - (long)h * ref.ns);
+      const float* qr = ref.q + ((long)h * ref.t + i) * ref.Es + (long)c * ref.ds;
+      const float* kr = ref.k + ((long)h * ref.t + bj) * ref.Es + (long)c * ref.ds;
+      float dot = 0.f;
+      for (int e = lane; e < ref.ds; e += 64) dot += qr[e] * kr[e];
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
+      fix_j[nfix] = bj;
+      fix_v[nfix] = dot * ref.scale * ref.rq[((long)h * ref.t + i) * ref.ns + c] *
+                    ref.rk[((long)h * ref.t + bj) * ref.ns + c];
+      ++nfix;
+    }
+    for (int r = 0; r < nfix; ++r) m = fmaxf(m, fix_v[r]);
+  }
+  auto val = [&](int i) {
+    float v = s[i];
+    for (int r = 0; r < nfix; ++r) v = (i == fix_j[r]) ? fix_v[r] : v;
+    return v;
+  };
   float sum = 0.f;
-  for (int i = lane; i < t; i += 64) sum += expf(s[i] - m);
+  for (int i = lane; i < t; i += 64) sum += expf(val(i) - m);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
   const float inv = 1.f / sum;
-  for (int i = lane; i < ld; i += 64) P[row * ld + i] = from_f32<CT>(i < t ? expf(s[i] - m) * inv : 0.f);
+  for (int i = lane; i < ld; i += 64) P[row * ld + i] = from_f32<CT>(i < t ? expf(val(i) - m) * inv : 0.f);
 }
 
-// Merge split-N partials: O[h*t + i][c*2d + f] = sum_s 2^(m_s - M) O_s / sum_s 2^(m_s - M) l_s.
+// ---------------------------------------------------------------------------
+// Exact-logit refinement of the heaviest keys.  The flash pass computes
+// logits from fp16-rounded q and k; for the few keys that carry almost all of
+// a latent's attention mass those roundings (amplified by the d_l logit
+// scale) matter, so their logits are recomputed accurately and the softmax
+// weights corrected.  P X is linear in P, so replacing the weights of the
+// selected keys is exact for them; every other key keeps a weight below
+// 2^-REFINE_MARGIN of the row maximum.
+// ---------------------------------------------------------------------------
+constexpr float REFINE_MARGIN = 14.f;   // log2 units
+
+// Pick, per latent row, the R largest fp16 logits among the flash pass's
+// per-split candidates that lie within REFINE_MARGIN of the row maximum.
+__global__ void refine_select_kernel(const float* __restrict__ cval, const int* __restrict__ cidx,
+                                     const float* __restrict__ mpart, int S, long HCT, int C, int R,
+                                     int* __restrict__ ridx, float* __restrict__ rval) {
+  const long row = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if (row >= HCT) return;
+  float M = -INFINITY;
+  for (int s = 0; s < S; ++s) M = fmaxf(M, mpart[s * HCT + row]);
+  float bv[8];
+  int bi[8];
+  for (int q = 0; q < R; ++q) {
+    bv[q] = -INFINITY;
+    bi[q] = -1;
+  }
+  for (int s = 0; s < S; ++s) {
+    const float* cv = cval + (s * HCT + row) * C;
+    const int* ci = cidx + (s * HCT + row) * C;
+    for (int k = 0; k < C; ++k) {
+      float v = cv[k];
+      int id = ci[k];
+      if (id < 0 || !(v >= M - REFINE_MARGIN) || !(v > bv[R - 1])) continue;
+      for (int q = 0; q < R; ++q) {
+        if (v > bv[q]) {
+          const float tv = bv[q];
+          const int tid = bi[q];
+          bv[q] = v;
+          bi[q] = id;
+          v = tv;
+          id = tid;
+        }
+      }
+    }
+  }
+  for (int q = 0; q < R; ++q) {
+    ridx[row * R + q] = bi[q];
+    rval[row * R + q] = bv[q];
+  }
+}
+
+// Gather the selected keys' X rows.  fp16 compute: the RoPE-fixed key half is
+// split into high and low parts, Xc[slot] = [K_hi (d) | V (d) | K_lo (d)];
+// fp32 compute: Xc[slot] = [K (d) | V (d)].
+template <class IT, class CT>
+__global__ void refine_gather_kernel(const IT* __restrict__ K, const IT* __restrict__ V,
+                                     const float2* __restrict__ tab, const int* __restrict__ ridx, long N, int d,
+                                     int nc, long slots_per_hc, long total_slots, CT* __restrict__ Xc) {
+  constexpr bool SPLIT = sizeof(CT) == 2;
+  const int hh = d / 2, W = SPLIT ? 3 * d : 2 * d;
+  const long total = total_slots * hh;
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total; e += (long)gridDim.x * blockDim.x) {
+    const long slot = e / hh;
+    const int j = (int)(e - slot * hh);
+    const int h = (int)(slot / slots_per_hc) / nc;
+    const int n = ridx[slot];
+    CT* x = Xc + slot * W;
+    if (n < 0) {
+      x[j] = x[j + hh] = x[d + j] = x[d + j + hh] = (CT)0.f;
+      if (SPLIT) x[2 * d + j] = x[2 * d + j + hh] = (CT)0.f;
+      continue;
+    }
+    const IT* kr = K + ((long)h * N + n) * d;
+    const IT* vr = V + ((long)h * N + n) * d;
+    const float2 cs = tab[(long)n * hh + j];
+    const float a = to_f32(kr[j]), b = to_f32(kr[j + hh]);
+    const float y0 = a * cs.x + b * cs.y, y1 = b * cs.x - a * cs.y;
+    const CT h0 = (CT)y0, h1 = (CT)y1;
+    x[j] = h0;
+    x[j + hh] = h1;
+    if (SPLIT) {
+      x[2 * d + j] = (CT)(y0 - (float)h0);
+      x[2 * d + j + hh] = (CT)(y1 - (float)h1);
+    }
+    x[d + j] = (CT)to_f32(vr[j]);
+    x[d + j + hh] = (CT)to_f32(vr[j + hh]);
+  }
+}
+
+// Merge split-N partials into O[h*t + i][c*2d + f]:
+//   O = (sum_s 2^(m_s - M) O_s + sum_r D_r X_r) / (sum_s 2^(m_s - M) l_s + sum_r D_r)
+// where, for each refined key r, D_r = 2^(S_exact - M) - 2^(S_fp16 - M) swaps
+// its fp16-logit weight for the accurate one (R = 0: plain merge).
+struct RefineArgs {
+  int R, NP;
+  const int* ridx;          // [H*nc*t][R]
+  const float* rval;        // [H*nc*t][R]   fp16 logits used by the flash pass (log2 units)
+  const float2* rpart;      // [H*nc*t*R][NP] (dot, sum of squares) partials of the exact keys
+  const float* rq;          // [H*t][nc]     1 / ||q~||
+  const void* X;            // [H*N][2d]     the rows the flash pass multiplied by P
+  long N;
+  float scale_log2, l2_eps;
+};
+
 template <class CT>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ opart, const float* __restrict__ mpart,
                                                     const float* __restrict__ lpart, int S, int H, int nc, int t,
-                                                    int d2, CT* __restrict__ O) {
+                                                    int d2, CT* __restrict__ O, RefineArgs ra) {
+  __shared__ float sdelta[8];
   const long row = blockIdx.x;     // (h*nc + c)*t + i
   const long HCT = (long)H * nc * t;
   const int hc = (int)(row / t), i = (int)(row - (long)hc * t);
@@ -175,6 +365,23 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
     const float ms = mpart[s * HCT + row];
     if (ms != -INFINITY) L += exp2f(ms - M) * lpart[s * HCT + row];
   }
+  if ((int)threadIdx.x < ra.R) {
+    const int r = threadIdx.x;
+    float dl = 0.f;
+    if (ra.ridx[row * ra.R + r] >= 0) {
+      const float2* p = ra.rpart + (row * ra.R + r) * ra.NP;
+      float dot = 0.f, ss = 0.f;
+      for (int k = 0; k < ra.NP; ++k) {
+        dot += p[k].x;
+        ss += p[k].y;
+      }
+      const float sx = ra.scale_log2 * ra.rq[((long)h * t + i) * nc + c] * dot / fmaxf(sqrtf(ss), ra.l2_eps);
+      dl = exp2f(sx - M) - exp2f(ra.rval[row * ra.R + r] - M);
+    }
+    sdelta[r] = dl;
+  }
+  __syncthreads();
+  for (int r = 0; r < ra.R; ++r) L += sdelta[r];
   const float invL = 1.f / L;
   CT* dst = O + ((long)h * t + i) * ((long)nc * d2) + (long)c * d2;
   for (int f = threadIdx.x; f < d2; f += 256) {
@@ -182,6 +389,10 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
     for (int s = 0; s < S; ++s) {
       const float ms = mpart[s * HCT + row];
       if (ms != -INFINITY) acc += exp2f(ms - M) * opart[(s * HCT + row) * d2 + f];
+    }
+    for (int r = 0; r < ra.R; ++r) {
+      const int n = ra.ridx[row * ra.R + r];
+      if (n >= 0) acc += sdelta[r] * to_f32(((const CT*)ra.X)[((long)h * ra.N + n) * d2 + f]);
     }
     dst[f] = from_f32<CT>(acc * invL);
   }

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "../../include/still.h"
 #include "attn.hpp"
@@ -37,9 +38,77 @@ static still_status fail(still_status s, const char* fmt, ...) {
 
 static inline long rup(long x, long m) { return (x + m - 1) / m * m; }
 
+// ---------------------------------------------------------------------------
+// Optional per-class kernel timing with hipEvent pairs on the launch stream.
+// ---------------------------------------------------------------------------
+namespace timing {
+struct Rec {
+  int cls;
+  hipEvent_t a, b;
+};
+static unsigned mask = 0;   // bit c: record launches of class c
+static std::vector<Rec> pending;
+static std::vector<hipEvent_t> spare;
+static double ms[STILL_K_COUNT];
+static long long count[STILL_K_COUNT];
+
+static hipEvent_t get_event() {
+  if (!spare.empty()) {
+    hipEvent_t e = spare.back();
+    spare.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Fold the oldest `n` pending records into the totals (waits for them).
+static hipError_t harvest(size_t n) {
+  if (n > pending.size()) n = pending.size();
+  for (size_t i = 0; i < n; ++i) {
+    Rec& r = pending[i];
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e != hipSuccess) return e;
+    float t = 0.f;
+    e = hipEventElapsedTime(&t, r.a, r.b);
+    if (e != hipSuccess) return e;
+    ms[r.cls] += t;
+    count[r.cls] += 1;
+    spare.push_back(r.a);
+    spare.push_back(r.b);
+  }
+  pending.erase(pending.begin(), pending.begin() + n);
+  return hipSuccess;
+}
+
+struct Scope {
+  int cls;
+  hipStream_t st;
+  hipEvent_t a = nullptr;
+  Scope(int c, hipStream_t s) : cls(c), st(s) {
+    if (!(mask & (1u << c))) return;
+    if (pending.size() >= 8192) harvest(4096);
+    a = get_event();
+    if (a) hipEventRecord(a, st);
+  }
+  ~Scope() {
+    if (!a) return;
+    hipEvent_t b = get_event();
+    if (!b) return;
+    hipEventRecord(b, st);
+    pending.push_back({cls, a, b});
+  }
+};
+}  // namespace timing
+
+#define TIMED(cls) timing::Scope _timed_scope_##__LINE__((cls), st)
+
 constexpr int GEMM_BN = 128;   // column tile of every GEMM (two halves of 64 pairs)
 constexpr int ATT_TT = 128;    // latents per attention workgroup
 constexpr int ATT_NB = 64;     // keys per attention block
+constexpr int ATT_TOPK = 4;    // keys tracked per latent half-lane for logit refinement (bf16 mode)
+constexpr int REFINE_R = 4;    // keys per latent whose logits are recomputed accurately
 
 // ---------------------------------------------------------------------------
 // Derived dimensions and workspace layout
@@ -48,6 +117,7 @@ struct Dims {
   int H, d, D, d2, nc, dc, ns, ds, F, Ec, Es, t, tpad;
   long N, Npad;
   int np_c, np_s;       // sum-of-squares partials per (row, head)
+  int topk, R;          // logit refinement (0 in fp32 mode)
   int splits;           // split-N factor of the cross-attention
   long keys_per_split;
   size_t cs;            // bytes of the compute/storage type
@@ -57,6 +127,7 @@ struct Dims {
 struct Plan {
   size_t pq, tab_ck, tab_cq, tab_bk, tab_bq;
   size_t X, XT, Z, Y, q, partq, rq, O;
+  size_t Ylo, qex, cval, cidx, ridx, rval, Xc, rpart;   // logit refinement
   // union region: cross-attention key side ...
   size_t k, partk, rk, opart, mpart, lpart;
   // ... or self-attention / FFN buffers
@@ -115,6 +186,8 @@ static still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims*
   m->Npad = rup(N, 128);
   m->np_c = m->dc / GEMM_BN * 2;
   m->np_s = m->ns > 0 ? m->ds / GEMM_BN * 2 : 0;
+  m->topk = ATT_TOPK;
+  m->R = REFINE_R;
   m->splits = choose_splits(*m);
   m->keys_per_split = rup((m->N + m->splits - 1) / m->splits, ATT_NB);
   m->splits = (int)((m->N + m->keys_per_split - 1) / m->keys_per_split);
@@ -145,6 +218,19 @@ static Plan make_plan(const Dims& m) {
   p.partq = take(4ul * Ht * m.nc * m.np_c);
   p.rq = take(4ul * Ht * m.nc);
   p.O = take(cs * Ht * m.nc * m.d2);
+  if (m.R > 0) {
+    const long HCT = Ht * m.nc;
+    if (!m.fp32) {
+      p.Ylo = take(cs * Ht * m.D);
+      p.qex = take(4ul * Ht * m.Ec);
+    }
+    p.cval = take(4ul * m.splits * HCT * 2 * m.topk);
+    p.cidx = take(4ul * m.splits * HCT * 2 * m.topk);
+    p.ridx = take(4ul * HCT * m.R);
+    p.rval = take(4ul * HCT * m.R);
+    p.Xc = take(cs * HCT * m.R * (m.fp32 ? 2 : 3) * m.d);
+    p.rpart = take(8ul * HCT * m.R * (m.dc / 64));
+  }
   const size_t ubase = off;
   p.k = take(cs * HN * m.Ec);
   p.partk = take(4ul * HN * m.nc * m.np_c);
@@ -179,7 +265,8 @@ template <> struct Tile<f16> { static constexpr int BM = 128, BN = GEMM_BN, BK =
 template <> struct Tile<float> { static constexpr int BM = 128, BN = GEMM_BN, BK = 16; };
 
 template <class CT, class TA, class TB, class TC, class TBias, int EPI>
-static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st) {
+static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st, int cls = STILL_K_LATENT) {
+  timing::Scope ts(cls, st);
   return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
 }
 
@@ -210,9 +297,10 @@ template <class CT, int D2>
 static hipError_t launch_attn(const AttnArgs& a, int splits, hipStream_t st) {
   dim3 grid((a.t + ATT_TT - 1) / ATT_TT, a.H * a.nc, splits);
   if constexpr (sizeof(CT) == 2) {
-    hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, ATT_NB, 64, D2>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, ATT_NB, 64, D2, ATT_TOPK>), grid, dim3(256), 0, st, a);
   } else {
-    hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, (D2 > 256 ? 32 : ATT_NB), 32, D2>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, (D2 > 256 ? 32 : ATT_NB), 32, D2, ATT_TOPK>), grid, dim3(256),
+                       0, st, a);
   }
   return hipGetLastError();
 }
@@ -222,6 +310,7 @@ static still_status prepare_tables(const Dims& m, const Plan& p, char* ws, const
                                    double rope_theta, double cbase, bool rerotate, double* out_positions,
                                    hipStream_t st) {
   double* pq = (double*)(ws + p.pq);
+  TIMED(STILL_K_OTHER);
   hipLaunchKernelGGL(positions_kernel, dim3(1), dim3(256), 0, st, positions, m.N, m.t, pq, out_positions);
   HIP_TRY(hipGetLastError());
   auto table = [&](const double* pos, long R, int w, double base, size_t off) -> hipError_t {
@@ -270,18 +359,30 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
     while (RW > 8 && (size_t)RW * (m.d2 + 1) * m.cs > 32768) RW /= 2;
     const size_t lds = (size_t)RW * (m.d2 + 1) * m.cs;
     dim3 grid((unsigned)((m.Npad + RW - 1) / RW), m.H);
+    TIMED(STILL_K_OTHER);
     hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, tab_bk, m.N,
                        m.d, X, XT, m.Npad, RW);
     HIP_TRY(hipGetLastError());
   }
-  hipLaunchKernelGGL((init_z_kernel<IT>), dim3(grid1d(Ht * m.D)), dim3(256), 0, st, (const IT*)w->latents, Z, Ht * m.D);
+  {
+    TIMED(STILL_K_OTHER);
+    hipLaunchKernelGGL((init_z_kernel<IT>), dim3(grid1d(Ht * m.D)), dim3(256), 0, st, (const IT*)w->latents, Z, Ht * m.D);
+  }
   HIP_TRY(hipGetLastError());
   auto rmsnorm = [&]() -> hipError_t {
+    TIMED(STILL_K_OTHER);
     hipLaunchKernelGGL((rmsnorm_kernel<CT>), dim3((unsigned)((Ht + 3) / 4)), dim3(256), 0, st, Z, Y, Ht, m.D,
                        cfg->rms_eps);
     return hipGetLastError();
   };
+  auto rmsnorm_split = [&](f16* hi, f16* lo) -> hipError_t {
+    TIMED(STILL_K_OTHER);
+    hipLaunchKernelGGL(rmsnorm_split_kernel, dim3((unsigned)((Ht + 3) / 4)), dim3(256), 0, st, Z, hi, lo, Ht, m.D,
+                       cfg->rms_eps);
+    return hipGetLastError();
+  };
   auto finalize = [&](const float* part, long rows, int nh, int np, float* rn) -> hipError_t {
+    TIMED(STILL_K_OTHER);
     hipLaunchKernelGGL(finalize_norm_kernel, dim3(grid1d(rows * nh)), dim3(256), 0, st, part, rows, nh, np,
                        cfg->l2_eps, rn);
     return hipGetLastError();
@@ -291,16 +392,25 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
     const still_block_weights& bw = w->blocks[b];
     // ---------------- cross-attention: Z += CrossAttn(RMSNorm(Z), X)
     if (cfg->cross_every_block || b == 0) {
-      HIP_TRY(rmsnorm());
+      if constexpr (sizeof(CT) == 2) {
+        if (m.R > 0 && !m.fp32) HIP_TRY(rmsnorm_split((f16*)Y, (f16*)(ws + p.Ylo)));
+        else HIP_TRY(rmsnorm());
+      } else {
+        HIP_TRY(rmsnorm());
+      }
       {  // q = RoPE_c(q~) with q~ = Y W_Q^T + b_Q, plus ||q~||^2 partials
         GemmArgs g = gargs((int)Ht, m.Ec / 2, m.D, Y, m.D, bw.ca_wq, m.D, q, m.Ec);
+        if (m.R > 0 && !m.fp32) {   // Y split into hi + lo: accurate q~ (fp32 copy for the refinement)
+          g.A2 = ws + p.Ylo;
+          g.C2 = (float*)(ws + p.qex);
+        }
         g.bias = bw.ca_bq;
         g.hd = m.dc;
         g.tab = tab_cq;
         g.tab_mod = m.t;
         g.part = partq;
         g.ldpart = (long)m.nc * m.np_c;
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_QPROJ)));
       }
       {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
         GemmArgs g = gargs((int)HN, m.Ec / 2, m.d2, X, m.d2, bw.ca_wk, m.d2, k, m.Ec);
@@ -310,7 +420,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.tab_mod = (int)m.N;
         g.part = partk;
         g.ldpart = (long)m.nc * m.np_c;
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_KPROJ)));
       }
       HIP_TRY(finalize(partq, Ht, m.nc, m.np_c, rq));
       HIP_TRY(finalize(partk, HN, m.nc, m.np_c, rk));
@@ -336,13 +446,71 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         const float s = cfg->logit_scale_cross != 0.f ? cfg->logit_scale_cross : (float)m.dc;
         a.scale_log2 = s * LOG2E;
         a.keys_per_split = (int)m.keys_per_split;
+        a.cval = (float*)(ws + p.cval);
+        a.cidx = (int*)(ws + p.cidx);
         hipError_t e;
+        {
+        TIMED(STILL_K_CROSS_ATTN);
         if (m.d2 == 128) e = launch_attn<CT, 128>(a, m.splits, st);
         else if (m.d2 == 256) e = launch_attn<CT, 256>(a, m.splits, st);
         else e = launch_attn<CT, 512>(a, m.splits, st);
+        }
         HIP_TRY(e);
+        RefineArgs ra;
+        memset(&ra, 0, sizeof ra);
+        if (m.R > 0) {
+          constexpr bool SPLIT = sizeof(CT) == 2;   // fp16: [K_hi | V | K_lo], fp32: [K | V]
+          const int W = SPLIT ? 3 * m.d : 2 * m.d;
+          const long HCT = Ht * m.nc;
+          int* ridx = (int*)(ws + p.ridx);
+          {
+            TIMED(STILL_K_REFINE);
+            hipLaunchKernelGGL(refine_select_kernel, dim3((unsigned)((HCT + 255) / 256)), dim3(256), 0, st, a.cval,
+                               a.cidx, a.mpart, m.splits, HCT, 2 * m.topk, m.R, ridx, (float*)(ws + p.rval));
+            HIP_TRY(hipGetLastError());
+            hipLaunchKernelGGL((refine_gather_kernel<IT, CT>), dim3(grid1d(HCT * m.R * (m.d / 2))), dim3(256), 0,
+                               st, (const IT*)Kp, (const IT*)Vp, tab_bk, ridx, m.N, m.d, m.nc, (long)m.t * m.R,
+                               HCT * m.R, (CT*)(ws + p.Xc));
+            HIP_TRY(hipGetLastError());
+          }
+          {  // exact k~ of the selected keys: [K_hi | V | K_lo] [W_K | W_K(key half)]^T, dotted with q~
+            GemmArgs g = gargs(m.t * m.R, m.dc / 2, W, ws + p.Xc, W, bw.ca_wk, m.d2, nullptr, 0);
+            g.nb2 = m.nc;
+            g.sA1 = (long)m.nc * m.t * m.R * W;
+            g.sA2 = (long)m.t * m.R * W;
+            g.sB2 = (long)m.dc * m.d2;
+            g.bwrap = SPLIT ? m.d2 : 0;
+            g.bias = bw.ca_bk;
+            g.sBias2 = m.dc;
+            g.hd = m.dc;
+            g.tab = tab_ck;
+            g.ridx = ridx;
+            g.sI1 = (long)m.nc * m.t * m.R;
+            g.sI2 = (long)m.t * m.R;
+            g.R = m.R;
+            g.qex = SPLIT ? (const float*)(ws + p.qex) : (const float*)q;   // fp32 mode: q is exact fp32
+            g.ldqex = m.Ec;
+            g.sE1 = (long)m.t * m.Ec;
+            g.sE2 = m.dc;
+            g.rpart = (float2*)(ws + p.rpart);
+            g.sR1 = (long)m.nc * m.t * m.R * (m.dc / 64);
+            g.sR2 = (long)m.t * m.R * (m.dc / 64);
+            HIP_TRY((gemm<CT, CT, IT, float, IT, EPI_REFINE>(g, m.H * m.nc, st, STILL_K_REFINE)));
+          }
+          ra.R = m.R;
+          ra.NP = m.dc / 64;
+          ra.ridx = ridx;
+          ra.rval = (const float*)(ws + p.rval);
+          ra.rpart = (const float2*)(ws + p.rpart);
+          ra.rq = rq;
+          ra.X = X;
+          ra.N = m.N;
+          ra.scale_log2 = a.scale_log2;
+          ra.l2_eps = cfg->l2_eps;
+        }
+        TIMED(STILL_K_OTHER);
         hipLaunchKernelGGL((merge_kernel<CT>), dim3((unsigned)(Ht * m.nc)), dim3(256), 0, st, a.opart, a.mpart,
-                           a.lpart, m.splits, m.H, m.nc, m.t, m.d2, O);
+                           a.lpart, m.splits, m.H, m.nc, m.t, m.d2, O, ra);
         HIP_TRY(hipGetLastError());
       }
       {  // head_c = O_c W_V,c^T   (batched over cross heads c)
@@ -390,6 +558,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.sC1 = (long)m.Es * m.tpad;
         HIP_TRY((gemm<CT, IT, CT, CT, IT, EPI_STORE>(g, m.H, st)));
         if (m.tpad > m.t) {
+          TIMED(STILL_K_OTHER);
           hipLaunchKernelGGL((zero_cols_kernel<CT>), dim3(grid1d((long)m.H * m.Es * (m.tpad - m.t))), dim3(256), 0,
                              st, vT, (long)m.H * m.Es, m.tpad, m.t, m.tpad);
           HIP_TRY(hipGetLastError());
@@ -417,8 +586,24 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.sK2 = 1;
         HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_SCALE>(g, m.H * m.ns, st)));
       }
+      {
+      TIMED(STILL_K_OTHER);
+      SoftmaxRefine sr;
+      memset(&sr, 0, sizeof sr);
+      if (m.fp32) {   // fp32 mode: q, k already fp32 -> recompute each row's top logits
+        sr.q = (const float*)qs;
+        sr.k = (const float*)ks;
+        sr.rq = rqs;
+        sr.rk = rks;
+        sr.Es = m.Es;
+        sr.ds = m.ds;
+        sr.ns = m.ns;
+        sr.t = m.t;
+        sr.scale = cfg->logit_scale_self != 0.f ? cfg->logit_scale_self : (float)m.ds;
+      }
       hipLaunchKernelGGL((softmax_rows_kernel<CT>), dim3((unsigned)(((long)m.H * m.ns * m.t + 3) / 4)), dim3(256), 0,
-                         st, Ssa, Psa, (long)m.H * m.ns * m.t, m.t, m.tpad);
+                         st, Ssa, Psa, (long)m.H * m.ns * m.t, m.t, m.tpad, sr);
+      }
       HIP_TRY(hipGetLastError());
       {  // O = P v per (h, c)
         GemmArgs g = gargs(m.t, m.ds, m.tpad, Psa, m.tpad, vT, m.tpad, Osa, m.Es);
@@ -608,5 +793,29 @@ const char* still_status_string(int32_t s) {
 const char* still_last_error(void) { return g_last_error.c_str(); }
 
 const char* still_version(void) { return "still-mi355x 0.1 (gfx950)"; }
+
+still_status still_timing_enable(int32_t class_mask) {
+  timing::mask = (unsigned)class_mask & ((1u << STILL_K_COUNT) - 1u);
+  return STILL_OK;
+}
+
+still_status still_timing_reset(void) {
+  hipError_t e = timing::harvest(timing::pending.size());
+  for (int i = 0; i < STILL_K_COUNT; ++i) {
+    timing::ms[i] = 0.0;
+    timing::count[i] = 0;
+  }
+  if (e != hipSuccess) return fail(STILL_E_HIP, "timing reset: %s", hipGetErrorString(e));
+  return STILL_OK;
+}
+
+still_status still_timing_read(int32_t cls, double* total_ms, int64_t* launches) {
+  if (cls < 0 || cls >= STILL_K_COUNT || !total_ms || !launches) return fail(STILL_E_INVAL, "bad timing query");
+  hipError_t e = timing::harvest(timing::pending.size());
+  if (e != hipSuccess) return fail(STILL_E_HIP, "timing read: %s", hipGetErrorString(e));
+  *total_ms = timing::ms[cls];
+  *launches = timing::count[cls];
+  return STILL_OK;
+}
 
 }  // extern "C"

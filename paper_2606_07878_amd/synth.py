@@ -117,3 +117,46 @@ def as_f64(d: dict) -> dict:
     """float64 views of every uint16 (bf16) entry; other entries passed through."""
     return {k: (bf16_value(v) if isinstance(v, np.ndarray) and v.dtype == np.uint16 else v)
             for k, v in d.items()}
+
+
+# ----------------------------------------------------------------------------
+# On-device generator for benchmark-sized stacks (same recipe, torch Philox
+# streams instead of numpy PCG64, so values differ from the numpy generator).
+# ----------------------------------------------------------------------------
+
+def _tgen(device, seed: int, layer: int, stream: int):
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed((seed * 1_000_003 + layer) * 101 + stream)
+    return g
+
+
+def make_layer_torch(w: Workload, layer: int, device, dtype=None, n_tokens: int | None = None,
+                     positions=None):
+    """(K, V, positions, weights) for one layer as device tensors (bf16 by default)."""
+    import torch
+    dtype = dtype or torch.bfloat16
+    cfg = w.cfg
+    H, d = cfg.n_kv_heads, cfg.head_dim
+    N = n_tokens if n_tokens is not None else w.n_tokens
+    if positions is None:
+        positions = torch.arange(N, dtype=torch.float64, device=device)
+    k_free = torch.randn(H, N, d, generator=_tgen(device, w.seed, layer, 0), device=device, dtype=torch.float32)
+    if w.outlier_channels:
+        g2 = _tgen(device, w.seed, layer, 2)
+        for h in range(H):
+            ch = torch.randperm(d, generator=g2, device=device)[: w.outlier_channels]
+            k_free[h][:, ch] *= w.outlier_scale
+    half = d // 2
+    inv = torch.pow(torch.tensor(float(w.rope_theta), dtype=torch.float64, device=device),
+                    -torch.arange(0, d, 2, dtype=torch.float64, device=device) / d)
+    ang = positions[:, None] * inv[None, :]
+    c, s = torch.cos(ang).float(), torch.sin(ang).float()
+    a, b = k_free[..., :half], k_free[..., half:]
+    K = torch.cat([a * c - b * s, b * c + a * s], dim=-1).to(dtype)
+    V = torch.randn(H, N, d, generator=_tgen(device, w.seed, layer, 1), device=device).to(dtype)
+    g3 = _tgen(device, w.seed, layer, 3)
+    from .configs import layer_shapes
+    weights = {k: (torch.randn(*shape, generator=g3, device=device) * WEIGHT_STD).to(dtype)
+               for k, shape in layer_shapes(cfg, w.t).items()}
+    return K, V, positions, weights
