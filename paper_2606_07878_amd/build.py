@@ -15,7 +15,9 @@ HEADERS = [os.path.join(PKG, "csrc", f) for f in ("common.hpp", "gemm.hpp", "att
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          # keep hipcc from forming packed fp32 (v_pk_*_f32) instructions
-         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         # MFMA operands/results in VGPRs; AGPRs then serve as fast spill space
+         "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
 def build_library(verbose: bool = False) -> str:

@@ -3,19 +3,25 @@
 //
 //   A [M][K] row-major (K contiguous), B [N][K] row-major (the [out][in] weight
 //   layout), both converted to the compute type CT on their way into LDS.
-//   256 threads = 4 waves in a 2x2 grid; each wave owns a (BM/2) x (BN/2) block
-//   of 32x32 MFMA tiles; two LDS stages, one barrier per k step.
+//   256 threads = 4 waves in a 2x2 grid; each wave owns a (BM/2) x (BN/2)
+//   block of 32x32 MFMA tiles; two LDS stages, one barrier per k step.  The
+//   epilogue stages each wave's results through LDS so that global stores are
+//   16-byte vectors along contiguous output columns.
 //
-// Paired epilogues (PAIR, SWIGLU) need two columns of the result in the same
-// lane: the tile's BN columns are two halves of BN/2, half 0 holding the first
-// member of each pair and half 1 the second, and every wave owns the same
-// sub-range in both halves.
+// Column layout: the tile's BN columns are two halves of BN/2 and every wave
+// owns the same sub-range of BN/4 columns in both halves, so paired epilogues
+// find both members of a pair in the same lane:
 //   PAIR:   pair P -> columns (c*hd + j, c*hd + j + hd/2), c = P / (hd/2),
 //           j = P % (hd/2): rotate-half RoPE partners (optional rotation by a
 //           cos/sin table, optional bias, optional per-row sum of squares of
-//           the un-rotated biased values for the later L2 QK-norm).
+//           the un-rotated biased values for the later L2 QK-norm, optional
+//           fp32 copy of the result).
 //   SWIGLU: pair P -> row P of W_g (half 0) and of W_u (half 1);
 //           out[:, P] = SiLU(g) * u.
+//   REFINE: PAIR rotation of gathered key rows, dotted with a query row
+//           (partial dot products and sums of squares instead of a store).
+// Other epilogues: STORE (+bias), GELU (+bias), RESID (C += acc, fp32),
+// SCALE (acc * scale * rq[row] * rk[col]).
 #pragma once
 #include "common.hpp"
 
@@ -24,21 +30,27 @@ namespace still {
 enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_PAIR = 2, EPI_SWIGLU = 3, EPI_SCALE = 4, EPI_GELU = 5, EPI_REFINE = 6 };
 
 struct GemmArgs {
-  int M, N, K;   // N = output columns, or column pairs for PAIR / SWIGLU
+  int M, N, K;   // N = output columns, or column pairs for PAIR / SWIGLU / REFINE
   int nb2;       // batch index z -> (z / nb2, z % nb2), strides s*1, s*2 (elements)
   const void* A;
   const void* A2;      // optional low part of a split A operand: C = (A + A2) B^T, same layout as A
   long lda, sA1, sA2;
   const void* B;
-  const void* B2;  // SWIGLU: W_u
+  const void* B2;      // SWIGLU: W_u
   long ldb, sB1, sB2;
   int bwrap;           // B column k >= bwrap reads column k - bwrap (0 = off)
+  // Row grouping: with mgroups > 1 the M rows are mgroups groups of M/mgroups
+  // rows spaced mgstride apart, and a tile takes BM/mgroups rows of every
+  // group (rows of different groups that share per-row side data, such as a
+  // rotation table row, then meet in one tile).
+  int mgroups;
+  long mgstride;
   void* C;
   long ldc, sC1, sC2;
   const void* bias;    // per output column, NULL = none
   long sBias2;         // bias offset per unit of the inner batch index
-  int hd;              // PAIR: head width
-  const float2* tab;   // PAIR: rotation table, row (r % tab_mod), entry [row*hd/2 + j]; NULL = none
+  int hd;              // PAIR / REFINE: head width
+  const float2* tab;   // rotation table, row (r % tab_mod) (REFINE: row ridx[r]), entry [row*hd/2 + j]; NULL = none
   int tab_mod;
   float* part;         // PAIR: per-row sum-of-squares partials, NULL = none
   long ldpart;
@@ -48,6 +60,8 @@ struct GemmArgs {
   // dots with qex row i and writes (dot, sum of squares) partials.
   const int* ridx;
   long sI1, sI2;
+  const int* crow;     // REFINE: compacted work list, row r -> candidate slot crow[r] (batch strides sI1, sI2)
+  const int* mcount;   // optional per-batch row count (device), overrides M; tiles past it exit at once
   int R;
   const float* qex;
   long ldqex, sE1, sE2;
@@ -63,6 +77,25 @@ struct GemmArgs {
 __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
 __device__ __forceinline__ float gelu_f(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
 
+// 16-byte vector of n elements of T
+template <class T> struct Vec16 {
+  static constexpr int n = 16 / sizeof(T);
+};
+
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): this wave's LDS traffic has completed
+  __builtin_amdgcn_wave_barrier();
+}
+
+// LDS arena: two operand stages, reused after the k loop for the epilogue
+// staging (4 waves x 32 rows x (BN/2 + 4) floats).
+template <int BM, int BN, int BK, class CT>
+constexpr int gemm_lds_bytes() {
+  const int ops = 2 * (BM + BN) * (BK + 16 / (int)sizeof(CT)) * (int)sizeof(CT);
+  const int stg = 4 * 32 * (BN / 2 + 4) * 4 + 2 * BM * 4;   // staging + REFINE row info
+  return ops > stg ? ops : stg;
+}
+
 template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   typedef Mma<CT> MM;
@@ -76,29 +109,55 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
   static_assert(AV >= 1 && BV >= 1 && BM * KV % 256 == 0 && BN * KV % 256 == 0, "tile/threads");
   static_assert(TN % 2 == 0, "BN must allow two column halves per wave");
+  // epilogue staging (per wave: 32 rows x TN*32 columns of fp32) must fit the arena
+  constexpr int WC = TN * 32;
+  constexpr int SLD = WC + 4;                  // staging row stride (floats)
+  static_assert(4 * 32 * SLD * 4 <= gemm_lds_bytes<BM, BN, BK, CT>(), "staging does not fit");
+  static_assert(WC == BN / 2, "wave column count");
 
-  __shared__ __attribute__((aligned(16))) CT As[2][BM * LR];
-  __shared__ __attribute__((aligned(16))) CT Bs[2][BN * LR];
+  __shared__ __attribute__((aligned(16))) unsigned char smem[gemm_lds_bytes<BM, BN, BK, CT>()];
+  CT* As = (CT*)smem;                          // [2][BM*LR]
+  CT* Bs = As + 2 * BM * LR;                   // [2][BN*LR]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int l32 = lane & 31, lg = lane >> 5;
 
-  // XCD-aware tile order: consecutive tiles of the N dimension (which share
-  // the A row block) stay on one XCD when the grid size allows it.
+  // Tile order: each XCD takes a contiguous range of tiles (workgroup ids are
+  // dealt to the 8 XCDs round robin), walked in groups of 8 M tiles x all N
+  // tiles, so the operand tiles the XCD's concurrent workgroups touch stay in
+  // its L2.
   const int gx = gridDim.x, gy = gridDim.y;
   int lin = blockIdx.x + gx * blockIdx.y;
   const int T = gx * gy;
   if ((T & 7) == 0) lin = (lin & 7) * (T >> 3) + (lin >> 3);
-  const int nt = lin % gx, mt = lin / gx;
+  constexpr int GM = 8;
+  const int grp = lin / (GM * gx), gm0 = grp * GM;
+  const int gsz = min(GM, gy - gm0);
+  const int inl = lin - grp * GM * gx;
+  const int mt = gm0 + inl % gsz, nt = inl / gsz;
 
   const int bz = blockIdx.z, b1 = bz / g.nb2, b2 = bz - b1 * g.nb2;
+  const int M = g.mcount ? g.mcount[bz] : g.M;
+  if (mt * BM >= M) return;   // whole workgroup past the (device-side) row count
   const TA* A = (const TA*)g.A + b1 * g.sA1 + b2 * g.sA2;
   const TB* B = (const TB*)g.B + b1 * g.sB1 + b2 * g.sB2;
   const TB* B2 = PAIRED && g.B2 ? (const TB*)g.B2 + b1 * g.sB1 + b2 * g.sB2 : nullptr;
-  const int M = g.M, N = g.N, K = g.K;
+  const int N = g.N, K = g.K;
   const int m0 = mt * BM;
   const int hh = g.hd >> 1;
+  const int mg = g.mgroups > 1 ? g.mgroups : 1;
+  const int RG = BM / mg;                      // rows per group in a tile
+  const int Mg = M / mg;                       // rows per group
+  // global row of tile-local row lr, or -1 past the end
+  auto grow = [&](int lr) -> long {
+    if (mg == 1) {
+      const int r = m0 + lr;
+      return r < M ? r : -1;
+    }
+    const int grp = lr / RG, rr = mt * RG + (lr - grp * RG);
+    return rr < Mg ? (long)grp * g.mgstride + rr : -1;
+  };
 
   // global -> register staging
   frag ra[AV], rb[BV];
@@ -129,8 +188,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < AV; ++i) {
       const int v = tid + i * 256, r = v / KV, kk = (v % KV) * E;
-      const int gr = m0 + r, gk = k0 + kk;
-      ra[i] = (gr < M && gk < K) ? VecLoad<CT, TA>::load(Ap + (long)gr * g.lda + gk) : zero_frag<CT>();
+      const long gr = grow(r);
+      const int gk = k0 + kk;
+      ra[i] = (gr >= 0 && gk < K) ? VecLoad<CT, TA>::load(Ap + gr * g.lda + gk) : zero_frag<CT>();
     }
 #pragma unroll
     for (int i = 0; i < BV; ++i) {
@@ -144,12 +204,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < AV; ++i) {
       const int v = tid + i * 256, r = v / KV, kk = (v % KV) * E;
-      *(frag*)&As[buf][r * LR + kk] = ra[i];
+      *(frag*)&As[buf * BM * LR + r * LR + kk] = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < BV; ++i) {
       const int v = tid + i * 256, r = v / KV, kk = (v % KV) * E;
-      *(frag*)&Bs[buf][r * LR + kk] = rb[i];
+      *(frag*)&Bs[buf * BN * LR + r * LR + kk] = rb[i];
     }
   };
 
@@ -177,15 +237,17 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       if (kn < nk1) load_stage(kn * BK, A);
       else load_stage((kn - nk1) * BK, Alo);
     }
+    const CT* Ac = As + cur * BM * LR;
+    const CT* Bc = Bs + cur * BN * LR;
 #pragma unroll
     for (int ks = 0; ks < BK / (2 * E); ++ks) {
       frag af[TM], bfr[TN];
 #pragma unroll
       for (int a = 0; a < TM; ++a)
-        af[a] = *(const frag*)&As[cur][(wm * (BM / 2) + a * 32 + l32) * LR + ks * 2 * E + lg * E];
+        af[a] = *(const frag*)&Ac[(wm * (BM / 2) + a * 32 + l32) * LR + ks * 2 * E + lg * E];
 #pragma unroll
       for (int b = 0; b < TN; ++b)
-        bfr[b] = *(const frag*)&Bs[cur][(col_base(b) + l32) * LR + ks * 2 * E + lg * E];
+        bfr[b] = *(const frag*)&Bc[(col_base(b) + l32) * LR + ks * 2 * E + lg * E];
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
@@ -196,101 +258,184 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   }
 
   // ------------------------------------------------------------------ epilogue
+  // Per 32-row slice a of the wave's block: values -> LDS staging (fp32, the
+  // wave's private region) -> contiguous runs of output columns -> 16-byte
+  // stores.  Output columns of the wave's run q (q = 0, 1: the two halves):
+  //   plain:  nt*BN + q*BN/2 + wn*BN/4 + [0, BN/4)
+  //   PAIR:   c*hd + j0 + q*hd/2 + [0, BN/4)  for the wave's pairs P0..P0+BN/4-1
+  //   SWIGLU: P0 + [0, BN/4) (one run)
+  float* stg = (float*)smem + wave * 32 * SLD;
   TC* C = (TC*)g.C + b1 * g.sC1 + b2 * g.sC2;
   const TBias* bias = g.bias ? (const TBias*)g.bias + b2 * g.sBias2 : nullptr;
-  if constexpr (!PAIRED) {
+  const int P0 = nt * (BN / 2) + wn * (BN / 4);           // first pair of the wave (paired kinds)
+  const int pc = PAIRED ? P0 / (hh > 0 ? hh : 1) : 0;     // head of the wave's pairs (PAIR, REFINE)
+  const int pj0 = PAIRED ? P0 - pc * hh : 0;
+  constexpr int RUN = BN / 4;
+  // columns of run q, element x: global output column and validity
+  auto run_col = [&](int q, int x) -> long {
+    if constexpr (EPI == EPI_PAIR) return (long)pc * g.hd + pj0 + q * hh + x;
+    else if constexpr (EPI == EPI_SWIGLU) return (long)P0 + x;
+    else return (long)nt * BN + q * (BN / 2) + wn * (BN / 4) + x;
+  };
+
+  float ss[TM][16], dd[TM][16];
 #pragma unroll
-    for (int a = 0; a < TM; ++a)
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) ss[a][j] = dd[a][j] = 0.f;
+
+  const int* ridx = (EPI == EPI_REFINE) ? g.ridx + b1 * g.sI1 + b2 * g.sI2 : nullptr;
+  const int* crow = (EPI == EPI_REFINE && g.crow) ? g.crow + b1 * g.sI1 + b2 * g.sI2 : nullptr;
+  // REFINE: slot and key of every tile row, read once into LDS (after the
+  // staging area) instead of per element
+  int* rslot = (int*)((float*)smem + 4 * 32 * SLD);
+  int* rkey = rslot + BM;
+  if constexpr (EPI == EPI_REFINE) {
+    for (int lr = tid; lr < BM; lr += 256) {
+      const long r = grow(lr);
+      const int slot = r < 0 ? 0 : (crow ? crow[r] : (int)r);
+      rslot[lr] = slot;
+      const int key = r < 0 ? -1 : ridx[slot];
+      rkey[lr] = key < 0 ? 0 : key;
+    }
+    __syncthreads();
+  }
+  const float* rqv = (EPI == EPI_SCALE) ? g.rq + b1 * g.sQ1 + b2 * g.sQ2 : nullptr;
+  const float* rkv = (EPI == EPI_SCALE) ? g.rk + b1 * g.sK1 + b2 * g.sK2 : nullptr;
+
+#pragma unroll
+  for (int a = 0; a < TM; ++a) {
+    const int lbase = wm * (BM / 2) + a * 32;    // tile-local first row of the slice
+    // ---- 1. values into the staging slice
+    if constexpr (!PAIRED) {
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
         const int col = nt * BN + col_base(b) + l32;
-        if (col >= N) continue;
-        const float bv = bias ? to_f32(bias[col]) : 0.f;
+        const float bv = (bias && col < N) ? to_f32(bias[col]) : 0.f;
+        const float rk = (EPI == EPI_SCALE && col < N) ? rkv[(long)col * g.ldrk] : 0.f;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const int r = m0 + wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3);
-          if (r >= M) continue;
+          const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
           float v = acc[a][b][j];
-          TC* dst = C + (long)r * g.ldc + col;
-          if constexpr (EPI == EPI_RESID) {
-            *dst = from_f32<TC>(to_f32(*dst) + v);
-          } else if constexpr (EPI == EPI_SCALE) {
-            const float* rq = g.rq + b1 * g.sQ1 + b2 * g.sQ2;
-            const float* rk = g.rk + b1 * g.sK1 + b2 * g.sK2;
-            *dst = from_f32<TC>(v * g.scale * rq[(long)r * g.ldrq] * rk[(long)col * g.ldrk]);
+          if constexpr (EPI == EPI_SCALE) {
+            const long r = grow(lbase + rl);
+            v = (r >= 0 && col < N) ? v * g.scale * rqv[r * g.ldrq] * rk : 0.f;
           } else if constexpr (EPI == EPI_GELU) {
-            *dst = from_f32<TC>(gelu_f(v + bv));
+            v = gelu_f(v + bv);
+          } else if constexpr (EPI != EPI_RESID) {
+            v = v + bv;
+          }
+          stg[rl * SLD + b * 32 + l32] = v;
+        }
+      }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+      for (int b = 0; b < TN / 2; ++b)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
+          stg[rl * SLD + b * 32 + l32] = silu_f(acc[a][b][j]) * acc[a][b + TN / 2][j];
+        }
+    } else {   // PAIR, REFINE
+#pragma unroll
+      for (int b = 0; b < TN / 2; ++b) {
+        const int x = b * 32 + l32;                 // position in the wave's run
+        const int jp = pj0 + x;
+        const bool pv = P0 + x < N;
+        const int col0 = pc * g.hd + jp, col1 = col0 + hh;
+        const float bv0 = (bias && pv) ? to_f32(bias[col0]) : 0.f;
+        const float bv1 = (bias && pv) ? to_f32(bias[col1]) : 0.f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
+          const long r = grow(lbase + rl);
+          const float v0 = acc[a][b][j] + bv0, v1 = acc[a][b + TN / 2][j] + bv1;
+          float y0 = v0, y1 = v1;
+          if (g.tab && pv && r >= 0) {
+            long trow;
+            if constexpr (EPI == EPI_REFINE) {
+              trow = rkey[lbase + rl];
+            } else {
+              trow = r % g.tab_mod;
+            }
+            const float2 cs = g.tab[trow * hh + jp];
+            y0 = v0 * cs.x - v1 * cs.y;
+            y1 = v1 * cs.x + v0 * cs.y;
+          }
+          if (pv) ss[a][j] += v0 * v0 + v1 * v1;
+          if constexpr (EPI == EPI_REFINE) {
+            if (pv && r >= 0) {
+              const float* qe = g.qex + b1 * g.sE1 + b2 * g.sE2 + (long)(rslot[lbase + rl] / g.R) * g.ldqex;
+              dd[a][j] += y0 * qe[col0] + y1 * qe[col1];
+            }
           } else {
-            *dst = from_f32<TC>(v + bv);
+            stg[rl * SLD + b * 32 + l32] = y0;
+            stg[rl * SLD + (b + TN / 2) * 32 + l32] = y1;
           }
         }
       }
-  } else {
-    float ss[TM][16], dd[TM][16];
-#pragma unroll
-    for (int a = 0; a < TM; ++a)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) ss[a][j] = dd[a][j] = 0.f;
-#pragma unroll
-    for (int b = 0; b < TN / 2; ++b) {
-      const int P = nt * (BN / 2) + wn * (BN / 4) + b * 32 + l32;
-      if (P >= N) continue;
-      if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-        for (int a = 0; a < TM; ++a)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int r = m0 + wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3);
-            if (r >= M) continue;
-            C[(long)r * g.ldc + P] = from_f32<TC>(silu_f(acc[a][b][j]) * acc[a][b + TN / 2][j]);
-          }
+    }
+    if constexpr (EPI == EPI_REFINE) continue;
+    wave_lds_fence();
+    // ---- 2. staged slice -> global, 16-byte vectors along each run
+    constexpr int NRUN = (EPI == EPI_SWIGLU) ? 1 : 2;
+    constexpr int VE = Vec16<TC>::n;
+    constexpr int VPR = RUN / VE;                  // vectors per run row
+    const bool vec_ok = (g.ldc % VE) == 0 && (((uintptr_t)C & 15) == 0);
+    for (int e = lane; e < 32 * NRUN * VPR; e += 64) {
+      const int rl = e / (NRUN * VPR);
+      const int rem = e - rl * NRUN * VPR;
+      const int q = rem / VPR, vx = (rem - q * VPR) * VE;
+      const long r = grow(lbase + rl);
+      if (r < 0) continue;
+      const float* src = stg + rl * SLD + q * RUN + vx;
+      const long col = run_col(q, vx);
+      TC* dst = C + r * g.ldc + col;
+      int nvalid;
+      if constexpr (PAIRED) {
+        nvalid = N - (P0 + vx);
       } else {
-        const int c = P / hh, jp = P - c * hh;
-        const int col0 = c * g.hd + jp, col1 = col0 + hh;
-        const int* ridx = (EPI == EPI_REFINE) ? g.ridx + b1 * g.sI1 + b2 * g.sI2 : nullptr;
-        const float bv0 = bias ? to_f32(bias[col0]) : 0.f;
-        const float bv1 = bias ? to_f32(bias[col1]) : 0.f;
+        nvalid = N - (int)col;
+      }
+      if (nvalid >= VE && vec_ok) {
+        if constexpr (EPI == EPI_RESID) {
+          f32x4 o = *(const f32x4*)dst;
 #pragma unroll
-        for (int a = 0; a < TM; ++a)
+          for (int u = 0; u < 4; ++u) o[u] += src[u];
+          *(f32x4*)dst = o;
+        } else {
+          TC tmp[VE];
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int r = m0 + wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3);
-            if (r >= M) continue;
-            const float v0 = acc[a][b][j] + bv0, v1 = acc[a][b + TN / 2][j] + bv1;
-            ss[a][j] += v0 * v0 + v1 * v1;
-            float y0 = v0, y1 = v1;
-            if (g.tab) {
-              long trow;
-              if constexpr (EPI == EPI_REFINE) {
-                const int key = ridx[r];
-                trow = key < 0 ? 0 : key;
-              } else {
-                trow = r % g.tab_mod;
-              }
-              const float2 cs = g.tab[trow * hh + jp];
-              y0 = v0 * cs.x - v1 * cs.y;
-              y1 = v1 * cs.x + v0 * cs.y;
-            }
-            if constexpr (EPI == EPI_REFINE) {
-              const int i = r / g.R;
-              const float* qe = g.qex + b1 * g.sE1 + b2 * g.sE2 + (long)i * g.ldqex;
-              dd[a][j] += y0 * qe[col0] + y1 * qe[col1];
-            } else {
-              C[(long)r * g.ldc + col0] = from_f32<TC>(y0);
-              C[(long)r * g.ldc + col1] = from_f32<TC>(y1);
-              if (g.C2) {
-                g.C2[(long)r * g.ldc + col0] = y0;
-                g.C2[(long)r * g.ldc + col1] = y1;
-              }
-            }
+          for (int u = 0; u < VE; ++u) tmp[u] = from_f32<TC>(src[u]);
+          *(uint4*)dst = *(const uint4*)tmp;
+        }
+      } else {
+        for (int u = 0; u < VE && u < nvalid; ++u) {
+          if constexpr (EPI == EPI_RESID) dst[u] = from_f32<TC>(to_f32(dst[u]) + src[u]);
+          else dst[u] = from_f32<TC>(src[u]);
+        }
+      }
+      if constexpr (EPI == EPI_PAIR) {
+        if (g.C2) {
+          float* d2 = g.C2 + r * g.ldc + col;
+          if (nvalid >= VE && vec_ok && (((uintptr_t)g.C2 & 15) == 0)) {
+#pragma unroll
+            for (int u = 0; u < VE; u += 4) *(f32x4*)(d2 + u) = *(const f32x4*)(src + u);
+          } else {
+            for (int u = 0; u < VE && u < nvalid; ++u) d2[u] = src[u];
           }
+        }
       }
     }
-    if constexpr (EPI == EPI_REFINE) {
-      const int P0 = nt * (BN / 2);
+    wave_lds_fence();
+  }
+
+  if constexpr (EPI == EPI_PAIR || EPI == EPI_REFINE) {
+    const bool want = (EPI == EPI_PAIR) ? (g.part != nullptr) : true;
+    if (want) {
+      // the wave's pairs lie inside one head c (hd/2 is a multiple of BN/2)
       const int nparts = (hh / (BN / 2)) * 2;
-      const int pidx = (P0 / (BN / 2)) * 2 + wn;
-      float2* rp = g.rpart + b1 * g.sR1 + b2 * g.sR2;
+      const int pidx = (pj0 / (BN / 2)) * 2 + wn;
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
@@ -299,33 +444,19 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
           for (int o = 1; o < 32; o <<= 1) {
             s += __shfl_xor(s, o);
-            q += __shfl_xor(q, o);
+            if constexpr (EPI == EPI_REFINE) q += __shfl_xor(q, o);
           }
-          const int r = m0 + wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3);
-          if (l32 == 0 && r < M) rp[(long)r * nparts + pidx] = make_float2(q, s);
+          const long r = grow(wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3));
+          if (l32 == 0 && r >= 0) {
+            if constexpr (EPI == EPI_REFINE) {
+              float2* rp = g.rpart + b1 * g.sR1 + b2 * g.sR2;
+              rp[(long)rslot[wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3)] * nparts + pidx] =
+                  make_float2(q, s);
+            } else {
+              g.part[r * g.ldpart + pc * nparts + pidx] = s;
+            }
+          }
         }
-    }
-    if constexpr (EPI == EPI_PAIR) {
-      if (g.part) {
-        // the tile's pairs lie inside one head c (hd/2 is a multiple of BN/2)
-        const int P0 = nt * (BN / 2);
-        const int c = P0 / hh;
-        const int nparts = (hh / (BN / 2)) * 2;
-        const int pidx = ((P0 - c * hh) / (BN / 2)) * 2 + wn;
-#pragma unroll
-        for (int a = 0; a < TM; ++a)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            float s = ss[a][j];
-            s += __shfl_xor(s, 1);
-            s += __shfl_xor(s, 2);
-            s += __shfl_xor(s, 4);
-            s += __shfl_xor(s, 8);
-            s += __shfl_xor(s, 16);
-            const int r = m0 + wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3);
-            if (l32 == 0 && r < M) g.part[(long)r * g.ldpart + c * nparts + pidx] = s;
-          }
-      }
     }
   }
 }
@@ -334,7 +465,8 @@ template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, 
 hipError_t launch_gemm(const GemmArgs& g, int batch, hipStream_t st) {
   constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
   const int ntn = PAIRED ? (g.N + BN / 2 - 1) / (BN / 2) : (g.N + BN - 1) / BN;
-  const int ntm = (g.M + BM - 1) / BM;
+  const int mg = g.mgroups > 1 ? g.mgroups : 1;
+  const int ntm = mg == 1 ? (g.M + BM - 1) / BM : (g.M / mg + BM / mg - 1) / (BM / mg);
   if (ntn <= 0 || ntm <= 0 || batch <= 0) return hipSuccess;
   dim3 grid(ntn, ntm, batch);
   hipLaunchKernelGGL((gemm_kernel<CT, TA, TB, TC, TBias, EPI, BM, BN, BK>), grid, dim3(256), 0, st, g);

@@ -148,6 +148,24 @@ __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float* __restr
   }
 }
 
+// q[r][c*dc + j] *= rq[r][c] * scale, in place (fp16): folds the query's
+// QK-norm factor and the logit scale into the operand of the QK product.
+__global__ void qprescale_kernel(f16* __restrict__ q, const float* __restrict__ rq, long rows, int nc, int dc,
+                                 float scale) {
+  const long per_row = (long)nc * dc / 8;
+  const long total = rows * per_row;
+  for (long v = blockIdx.x * (long)blockDim.x + threadIdx.x; v < total; v += (long)gridDim.x * blockDim.x) {
+    const long r = v / per_row;
+    const int col = (int)(v - r * per_row) * 8;
+    const float f = rq[r * nc + col / dc] * scale;
+    half8* p = (half8*)(q + r * nc * (long)dc + col);
+    half8 x = *p;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = (f16)((float)x[i] * f);
+    *p = x;
+  }
+}
+
 // rn[r][c] = 1 / max(sqrt(sum_p part[r][c][p]), eps)   (QK-norm factors)
 __global__ void finalize_norm_kernel(const float* __restrict__ part, long rows, int nh, int np,
                                      float eps, float* __restrict__ rn) {
@@ -254,7 +272,7 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* __restri
 // selected keys is exact for them; every other key keeps a weight below
 // 2^-REFINE_MARGIN of the row maximum.
 // ---------------------------------------------------------------------------
-constexpr float REFINE_MARGIN = 14.f;   // log2 units
+constexpr float REFINE_MARGIN = 10.f;   // log2 units
 
 // Pick, per latent row, the R largest fp16 logits among the flash pass's
 // per-split candidates that lie within REFINE_MARGIN of the row maximum.
@@ -296,32 +314,58 @@ __global__ void refine_select_kernel(const float* __restrict__ cval, const int* 
   }
 }
 
-// Gather the selected keys' X rows.  fp16 compute: the RoPE-fixed key half is
-// split into high and low parts, Xc[slot] = [K_hi (d) | V (d) | K_lo (d)];
-// fp32 compute: Xc[slot] = [K (d) | V (d)].
+// Pack the non-empty refinement slots of each (KV head, cross head): for
+// batch b, crow[b][0..count[b]) lists the slots (index into the b's t*R slots)
+// whose key is >= 0, in slot order.  One workgroup per batch.
+__global__ __launch_bounds__(256) void refine_compact_kernel(const int* __restrict__ ridx, int TR,
+                                                             int* __restrict__ crow, int* __restrict__ count) {
+  __shared__ int ssum[256];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int per = (TR + 255) / 256;
+  const int lo = min(TR, tid * per), hi = min(TR, lo + per);
+  const int* rb = ridx + (long)b * TR;
+  int n = 0;
+  for (int i = lo; i < hi; ++i) n += rb[i] >= 0;
+  ssum[tid] = n;
+  __syncthreads();
+  for (int o = 1; o < 256; o <<= 1) {   // inclusive scan
+    const int v = tid >= o ? ssum[tid - o] : 0;
+    __syncthreads();
+    ssum[tid] += v;
+    __syncthreads();
+  }
+  int pos = ssum[tid] - n;
+  int* cb = crow + (long)b * TR;
+  for (int i = lo; i < hi; ++i)
+    if (rb[i] >= 0) cb[pos++] = i;
+  if (tid == 255) count[b] = ssum[255];
+}
+
+// Gather the X rows of the packed refinement slots.  fp16 compute: the
+// RoPE-fixed key half is split into high and low parts,
+// Xc[b][j] = [K_hi (d) | V (d) | K_lo (d)]; fp32 compute: Xc[b][j] = [K (d) | V (d)].
 template <class IT, class CT>
 __global__ void refine_gather_kernel(const IT* __restrict__ K, const IT* __restrict__ V,
-                                     const float2* __restrict__ tab, const int* __restrict__ ridx, long N, int d,
-                                     int nc, long slots_per_hc, long total_slots, CT* __restrict__ Xc) {
+                                     const float2* __restrict__ tab, const int* __restrict__ ridx,
+                                     const int* __restrict__ crow, const int* __restrict__ count, long N, int d,
+                                     int nc, int TR, int nbatch, CT* __restrict__ Xc) {
   constexpr bool SPLIT = sizeof(CT) == 2;
   const int hh = d / 2, W = SPLIT ? 3 * d : 2 * d;
-  const long total = total_slots * hh;
+  const long total = (long)nbatch * TR * hh;
   for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total; e += (long)gridDim.x * blockDim.x) {
-    const long slot = e / hh;
-    const int j = (int)(e - slot * hh);
-    const int h = (int)(slot / slots_per_hc) / nc;
-    const int n = ridx[slot];
-    CT* x = Xc + slot * W;
-    if (n < 0) {
-      x[j] = x[j + hh] = x[d + j] = x[d + j + hh] = (CT)0.f;
-      if (SPLIT) x[2 * d + j] = x[2 * d + j + hh] = (CT)0.f;
-      continue;
-    }
+    const long row = e / hh;                 // b * TR + j
+    const int j = (int)(e - row * hh);
+    const int b = (int)(row / TR), jr = (int)(row - (long)b * TR);
+    if (jr >= count[b]) continue;
+    const int h = b / nc;
+    const int slot = crow[row];
+    const int n = ridx[(long)b * TR + slot];
+    CT* x = Xc + row * W;
     const IT* kr = K + ((long)h * N + n) * d;
     const IT* vr = V + ((long)h * N + n) * d;
     const float2 cs = tab[(long)n * hh + j];
-    const float a = to_f32(kr[j]), b = to_f32(kr[j + hh]);
-    const float y0 = a * cs.x + b * cs.y, y1 = b * cs.x - a * cs.y;
+    const float a = to_f32(kr[j]), bb = to_f32(kr[j + hh]);
+    const float y0 = a * cs.x + bb * cs.y, y1 = bb * cs.x - a * cs.y;
     const CT h0 = (CT)y0, h1 = (CT)y1;
     x[j] = h0;
     x[j + hh] = h1;

@@ -107,7 +107,9 @@ struct Scope {
 constexpr int GEMM_BN = 128;   // column tile of every GEMM (two halves of 64 pairs)
 constexpr int ATT_TT = 128;    // latents per attention workgroup
 constexpr int ATT_NB = 64;     // keys per attention block
-constexpr int ATT_TOPK = 4;    // keys tracked per latent half-lane for logit refinement (bf16 mode)
+constexpr int ATT_TOPK = 4;    // keys tracked per latent half-lane for logit refinement (fp32 kernel)
+constexpr int XATT_KB = 256;   // keys per block of the fp16 cross-attention kernel
+constexpr int XATT_TOPK = 4;   // keys tracked per (latent, wave, lane half) by the fp16 kernel
 constexpr int REFINE_R = 4;    // keys per latent whose logits are recomputed accurately
 
 // ---------------------------------------------------------------------------
@@ -117,7 +119,9 @@ struct Dims {
   int H, d, D, d2, nc, dc, ns, ds, F, Ec, Es, t, tpad;
   long N, Npad;
   int np_c, np_s;       // sum-of-squares partials per (row, head)
-  int topk, R;          // logit refinement (0 in fp32 mode)
+  int topk, R;          // logit refinement
+  int ncand;            // candidate keys per (split, latent row) written by the attention kernel
+  int att_tt;           // latents per attention workgroup
   int splits;           // split-N factor of the cross-attention
   long keys_per_split;
   size_t cs;            // bytes of the compute/storage type
@@ -127,7 +131,7 @@ struct Dims {
 struct Plan {
   size_t pq, tab_ck, tab_cq, tab_bk, tab_bq;
   size_t X, XT, Z, Y, q, partq, rq, O;
-  size_t Ylo, qex, cval, cidx, ridx, rval, Xc, rpart;   // logit refinement
+  size_t Ylo, qex, cval, cidx, ridx, rval, Xc, rpart, crow, ccount;   // logit refinement
   // union region: cross-attention key side ...
   size_t k, partk, rk, opart, mpart, lpart;
   // ... or self-attention / FFN buffers
@@ -135,10 +139,13 @@ struct Plan {
   size_t total;
 };
 
+static int key_block(const Dims& m) { return m.fp32 ? ATT_NB : XATT_KB; }
+
 static int choose_splits(const Dims& m) {
-  const long wgs = (long)((m.t + ATT_TT - 1) / ATT_TT) * m.H * m.nc;
-  const long nblocks = (m.N + ATT_NB - 1) / ATT_NB;
-  long s = (1024 + wgs - 1) / wgs;            // aim for >= 4 workgroups per CU
+  const long wgs = (long)((m.t + m.att_tt - 1) / m.att_tt) * m.H * m.nc;
+  const long nblocks = (m.N + key_block(m) - 1) / key_block(m);
+  // fp16 kernel: one workgroup per CU, aim for >= 2 per CU; fp32: >= 4
+  long s = ((m.fp32 ? 1024 : 512) + wgs - 1) / wgs;
   if (s > nblocks) s = nblocks;
   if (s < 1) s = 1;
   return (int)s;
@@ -183,13 +190,15 @@ static still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims*
   if ((long)m->H * N > (long)GEMM_BN * 65535L)
     return fail(STILL_E_UNSUPPORTED, "H*N = %lld exceeds the supported %ld rows", (long long)(m->H * N), (long)GEMM_BN * 65535L);
   m->tpad = (int)rup(t, 64);
-  m->Npad = rup(N, 128);
+  m->Npad = rup(N, 256);
   m->np_c = m->dc / GEMM_BN * 2;
   m->np_s = m->ns > 0 ? m->ds / GEMM_BN * 2 : 0;
-  m->topk = ATT_TOPK;
+  m->topk = m->fp32 ? ATT_TOPK : XATT_TOPK;
+  m->ncand = m->fp32 ? 2 * ATT_TOPK : 8 * XATT_TOPK;
   m->R = REFINE_R;
+  m->att_tt = (m->fp32 || m->d2 <= 256) ? 128 : 64;
   m->splits = choose_splits(*m);
-  m->keys_per_split = rup((m->N + m->splits - 1) / m->splits, ATT_NB);
+  m->keys_per_split = rup((m->N + m->splits - 1) / m->splits, key_block(*m));
   m->splits = (int)((m->N + m->keys_per_split - 1) / m->keys_per_split);
   return STILL_OK;
 }
@@ -224,12 +233,14 @@ static Plan make_plan(const Dims& m) {
       p.Ylo = take(cs * Ht * m.D);
       p.qex = take(4ul * Ht * m.Ec);
     }
-    p.cval = take(4ul * m.splits * HCT * 2 * m.topk);
-    p.cidx = take(4ul * m.splits * HCT * 2 * m.topk);
+    p.cval = take(4ul * m.splits * HCT * m.ncand);
+    p.cidx = take(4ul * m.splits * HCT * m.ncand);
     p.ridx = take(4ul * HCT * m.R);
     p.rval = take(4ul * HCT * m.R);
     p.Xc = take(cs * HCT * m.R * (m.fp32 ? 2 : 3) * m.d);
     p.rpart = take(8ul * HCT * m.R * (m.dc / 64));
+    p.crow = take(4ul * HCT * m.R);
+    p.ccount = take(4ul * m.H * m.nc);
   }
   const size_t ubase = off;
   p.k = take(cs * HN * m.Ec);
@@ -297,7 +308,11 @@ template <class CT, int D2>
 static hipError_t launch_attn(const AttnArgs& a, int splits, hipStream_t st) {
   dim3 grid((a.t + ATT_TT - 1) / ATT_TT, a.H * a.nc, splits);
   if constexpr (sizeof(CT) == 2) {
-    hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, ATT_NB, 64, D2, ATT_TOPK>), grid, dim3(256), 0, st, a);
+    constexpr int TT = D2 <= 256 ? 128 : 64;
+    const int ntt = (a.t + TT - 1) / TT;
+    constexpr int DK = D2 == 256 ? 32 : 64;   // register budget (no scratch spills)
+    hipLaunchKernelGGL((xattn_f16_kernel<TT, DK, D2, XATT_TOPK>), dim3(ntt * a.H * a.nc * splits), dim3(256), 0, st,
+                       a);
   } else {
     hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, (D2 > 256 ? 32 : ATT_NB), 32, D2, ATT_TOPK>), grid, dim3(256),
                        0, st, a);
@@ -414,6 +429,10 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
       }
       {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
         GemmArgs g = gargs((int)HN, m.Ec / 2, m.d2, X, m.d2, bw.ca_wk, m.d2, k, m.Ec);
+        if (Tile<CT>::BM % m.H == 0) {   // tiles span the same keys of every KV head: shared table rows
+          g.mgroups = m.H;
+          g.mgstride = m.N;
+        }
         g.bias = bw.ca_bk;
         g.hd = m.dc;
         g.tab = tab_ck;
@@ -424,6 +443,13 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
       }
       HIP_TRY(finalize(partq, Ht, m.nc, m.np_c, rq));
       HIP_TRY(finalize(partk, HN, m.nc, m.np_c, rk));
+      const float ca_scale = cfg->logit_scale_cross != 0.f ? cfg->logit_scale_cross : (float)m.dc;
+      if constexpr (sizeof(CT) == 2) {   // fold 1/||q~|| * scale * log2(e) into q for the fp16 kernel
+        TIMED(STILL_K_OTHER);
+        hipLaunchKernelGGL(qprescale_kernel, dim3(grid1d(Ht * m.Ec / 8)), dim3(256), 0, st, (f16*)q, rq, Ht, m.nc,
+                           m.dc, ca_scale * LOG2E);
+        HIP_TRY(hipGetLastError());
+      }
       {
         AttnArgs a;
         a.q = q;
@@ -443,8 +469,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         a.nc = m.nc;
         a.dc = m.dc;
         a.d2 = m.d2;
-        const float s = cfg->logit_scale_cross != 0.f ? cfg->logit_scale_cross : (float)m.dc;
-        a.scale_log2 = s * LOG2E;
+        a.scale_log2 = ca_scale * LOG2E;
         a.keys_per_split = (int)m.keys_per_split;
         a.cval = (float*)(ws + p.cval);
         a.cidx = (int*)(ws + p.cidx);
@@ -466,14 +491,19 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
           {
             TIMED(STILL_K_REFINE);
             hipLaunchKernelGGL(refine_select_kernel, dim3((unsigned)((HCT + 255) / 256)), dim3(256), 0, st, a.cval,
-                               a.cidx, a.mpart, m.splits, HCT, 2 * m.topk, m.R, ridx, (float*)(ws + p.rval));
+                               a.cidx, a.mpart, m.splits, HCT, m.ncand, m.R, ridx, (float*)(ws + p.rval));
+            HIP_TRY(hipGetLastError());
+            const int TR = m.t * m.R, NB = m.H * m.nc;
+            int* crow = (int*)(ws + p.crow);
+            int* ccount = (int*)(ws + p.ccount);
+            hipLaunchKernelGGL(refine_compact_kernel, dim3(NB), dim3(256), 0, st, ridx, TR, crow, ccount);
             HIP_TRY(hipGetLastError());
             hipLaunchKernelGGL((refine_gather_kernel<IT, CT>), dim3(grid1d(HCT * m.R * (m.d / 2))), dim3(256), 0,
-                               st, (const IT*)Kp, (const IT*)Vp, tab_bk, ridx, m.N, m.d, m.nc, (long)m.t * m.R,
-                               HCT * m.R, (CT*)(ws + p.Xc));
+                               st, (const IT*)Kp, (const IT*)Vp, tab_bk, ridx, crow, ccount, m.N, m.d, m.nc, TR, NB,
+                               (CT*)(ws + p.Xc));
             HIP_TRY(hipGetLastError());
           }
-          {  // exact k~ of the selected keys: [K_hi | V | K_lo] [W_K | W_K(key half)]^T, dotted with q~
+          {  // exact k~ of the packed keys: [K_hi | V | K_lo] [W_K | W_K(key half)]^T, dotted with q~
             GemmArgs g = gargs(m.t * m.R, m.dc / 2, W, ws + p.Xc, W, bw.ca_wk, m.d2, nullptr, 0);
             g.nb2 = m.nc;
             g.sA1 = (long)m.nc * m.t * m.R * W;
@@ -485,6 +515,8 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
             g.hd = m.dc;
             g.tab = tab_ck;
             g.ridx = ridx;
+            g.crow = (const int*)(ws + p.crow);
+            g.mcount = (const int*)(ws + p.ccount);
             g.sI1 = (long)m.nc * m.t * m.R;
             g.sI2 = (long)m.t * m.R;
             g.R = m.R;
