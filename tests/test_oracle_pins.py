@@ -228,10 +228,9 @@ def test_identity_init_is_near_pass_through(theta):
 
 # --------------------------------------------------------------------------- loop evaluation
 
-def _loop_layer(K, V, pos, theta, w, cfg, t):
+def _loop_layer(K, V, pos, theta, w, cfg, t, rerotate=True):
     """Whole layer with explicit Python loops (tiny sizes), written independently."""
     H, N, d = K.shape
-    D = cfg.latent_dim
     nc, dc, ns, ds = cfg.n_cross_heads, cfg.dc, cfg.n_self_heads, cfg.ds
 
     def lin(x, W, b=None):
@@ -265,57 +264,90 @@ def _loop_layer(K, V, pos, theta, w, cfg, t):
             out.append([sum(e[n] * vs[n][f] for n in range(len(vs))) / z for f in range(len(vs[0]))])
         return out
 
+    def add(Z, rows):
+        return [[a + b for a, b in zip(z, r)] for z, r in zip(Z, rows)]
+
     lo, hi = min(pos), max(pos)
-    pq = [lo + i * (hi - lo) / (t - 1) for i in range(t)]
+    pq = [lo + i * (hi - lo) / (t - 1) for i in range(t)] if t > 1 else [lo]
     Ck = np.zeros((H, t, d))
     Cv = np.zeros((H, t, d))
     for h in range(H):
         X = [rot(list(K[h, n]), pos[n], theta, -1) + list(V[h, n]) for n in range(N)]
         Z = [list(w["latents"][h, i]) for i in range(t)]
-        # cross-attention
-        Q = [rms(z) for z in Z]
-        cat = [[] for _ in range(t)]
-        for c in range(nc):
-            r = slice(c * dc, (c + 1) * dc)
-            qs = [rot(unit(lin(q, w["b0.ca_wq"][r], w["b0.ca_bq"][r])), pq[i], cfg.compactor_rope_base, 1)
-                  for i, q in enumerate(Q)]
-            ks = [rot(unit(lin(x, w["b0.ca_wk"][r], w["b0.ca_bk"][r])), pos[n], cfg.compactor_rope_base, 1)
-                  for n, x in enumerate(X)]
-            vs = [lin(x, w["b0.ca_wv"][r]) for x in X]
-            for i, o in enumerate(attend(qs, ks, vs, dc)):
-                cat[i] += o
-        Z = [[a + b for a, b in zip(z, lin(cat[i], w["b0.ca_wo"]))] for i, z in enumerate(Z)]
-        # self-attention
-        Y = [rms(z) for z in Z]
-        cat = [[] for _ in range(t)]
-        for c in range(ns):
-            r = slice(c * ds, (c + 1) * ds)
-            qs = [unit(lin(y, w["b0.sa_wq"][r], w["b0.sa_bq"][r])) for y in Y]
-            ks = [unit(lin(y, w["b0.sa_wk"][r], w["b0.sa_bk"][r])) for y in Y]
-            vs = [lin(y, w["b0.sa_wv"][r]) for y in Y]
-            for i, o in enumerate(attend(qs, ks, vs, ds)):
-                cat[i] += o
-        Z = [[a + b for a, b in zip(z, lin(cat[i], w["b0.sa_wo"]))] for i, z in enumerate(Z)]
-        # SwiGLU FFN
-        Y = [rms(z) for z in Z]
-        for i, y in enumerate(Y):
-            g, u = lin(y, w["b0.ffn_wg"]), lin(y, w["b0.ffn_wu"])
-            hdn = [gv / (1 + math.exp(-gv)) * uv for gv, uv in zip(g, u)]
-            Z[i] = [a + b for a, b in zip(Z[i], lin(hdn, w["b0.ffn_wd"]))]
+        for b in range(cfg.n_blocks):
+            B = f"b{b}."
+            if nc and (b == 0 or cfg.cross_every_block):
+                Q = [rms(z) for z in Z]
+                cat = [[] for _ in range(t)]
+                for c in range(nc):
+                    r = slice(c * dc, (c + 1) * dc)
+                    qs = [rot(unit(lin(q, w[B + "ca_wq"][r], w[B + "ca_bq"][r])), pq[i],
+                              cfg.compactor_rope_base, 1) for i, q in enumerate(Q)]
+                    ks = [rot(unit(lin(x, w[B + "ca_wk"][r], w[B + "ca_bk"][r])), pos[n],
+                              cfg.compactor_rope_base, 1) for n, x in enumerate(X)]
+                    vs = [lin(x, w[B + "ca_wv"][r]) for x in X]
+                    for i, o in enumerate(attend(qs, ks, vs, dc)):
+                        cat[i] += o
+                Z = add(Z, [lin(c_, w[B + "ca_wo"]) for c_ in cat])
+            if ns:
+                Y = [rms(z) for z in Z]
+                cat = [[] for _ in range(t)]
+                for c in range(ns):
+                    r = slice(c * ds, (c + 1) * ds)
+                    qs = [unit(lin(y, w[B + "sa_wq"][r], w[B + "sa_bq"][r])) for y in Y]
+                    ks = [unit(lin(y, w[B + "sa_wk"][r], w[B + "sa_bk"][r])) for y in Y]
+                    vs = [lin(y, w[B + "sa_wv"][r]) for y in Y]
+                    for i, o in enumerate(attend(qs, ks, vs, ds)):
+                        cat[i] += o
+                Z = add(Z, [lin(c_, w[B + "sa_wo"]) for c_ in cat])
+            if cfg.ffn_kind != configs.FFN_NONE:
+                Y = [rms(z) for z in Z]
+                upd = []
+                for y in Y:
+                    u = lin(y, w[B + "ffn_wu"])
+                    if cfg.ffn_kind == configs.FFN_SWIGLU:
+                        g = lin(y, w[B + "ffn_wg"])
+                        hdn = [gv / (1 + math.exp(-gv)) * uv for gv, uv in zip(g, u)]
+                    else:
+                        hdn = [0.5 * uv * (1 + math.erf(uv / math.sqrt(2))) for uv in u]
+                    upd.append(lin(hdn, w[B + "ffn_wd"]))
+                Z = add(Z, upd)
+        if cfg.final_norm:
+            Z = [rms(z) for z in Z]
         for i in range(t):
-            Ck[h, i] = rot(lin(Z[i], w["w_key"]), pq[i], theta, 1)
+            ck = lin(Z[i], w["w_key"])
+            Ck[h, i] = rot(ck, pq[i], theta, 1) if rerotate else ck
             Cv[h, i] = lin(Z[i], w["w_val"])
     return Ck, Cv, np.array(pq)
 
 
-def test_layer_matches_loop_evaluation():
-    cfg = tiny_cfg()
+LOOP_VARIANTS = {
+    "base": {},
+    "gelu_final_norm": dict(ffn_kind=configs.FFN_GELU, final_norm=1),
+    "two_blocks": dict(n_blocks=2),
+    "resampler": dict(n_blocks=2, cross_every_block=0, n_cross_heads=1),
+    "cross_only_one_head": dict(n_self_heads=0, ffn_kind=configs.FFN_NONE, n_cross_heads=1),
+}
+
+
+@pytest.mark.parametrize("variant", list(LOOP_VARIANTS))
+def test_layer_matches_loop_evaluation(variant, rerotate=True):
+    cfg = tiny_cfg(**LOOP_VARIANTS[variant])
     t, N = 3, 6
-    w = rand_weights(cfg, t, std=0.6)
-    K, V, pos, th = _layer_inputs(cfg, N, t)
-    ref = _loop_layer(K, V, pos, th, w, cfg, t)
-    got = O.compact_layer(K, V, pos, th, w, cfg, t)
+    w = rand_weights(cfg, t, std=0.6, rng=np.random.default_rng(11))
+    K, V, pos, th = _layer_inputs(cfg, N, t, rng=np.random.default_rng(12))
+    ref = _loop_layer(K, V, pos, th, w, cfg, t, rerotate=rerotate)
+    got = O.compact_layer(K, V, pos, th, w, cfg, t, rerotate=rerotate)
     for a, b in zip(got, ref):
+        np.testing.assert_allclose(a, b, rtol=1e-11, atol=1e-12)
+
+
+def test_layer_matches_loop_evaluation_no_rerotate_single_latent():
+    test_layer_matches_loop_evaluation("base", rerotate=False)
+    cfg = tiny_cfg()
+    w = rand_weights(cfg, 1, std=0.6, rng=np.random.default_rng(13))
+    K, V, pos, th = _layer_inputs(cfg, 5, 1, rng=np.random.default_rng(14))
+    for a, b in zip(O.compact_layer(K, V, pos, th, w, cfg, 1), _loop_layer(K, V, pos, th, w, cfg, 1)):
         np.testing.assert_allclose(a, b, rtol=1e-11, atol=1e-12)
 
 
