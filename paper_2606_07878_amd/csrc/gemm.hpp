@@ -4,9 +4,11 @@
 //   A [M][K] row-major (K contiguous), B [N][K] row-major (the [out][in] weight
 //   layout), both converted to the compute type CT on their way into LDS.
 //   256 threads = 4 waves in a 2x2 grid; each wave owns a (BM/2) x (BN/2)
-//   block of 32x32 MFMA tiles; two LDS stages, one barrier per k step.  The
-//   epilogue stages each wave's results through LDS so that global stores are
-//   16-byte vectors along contiguous output columns.
+//   block of 32x32 MFMA tiles; two LDS stages, one barrier per k step.  LDS
+//   rows are unpadded; the 16-byte units of a row are XOR-swizzled by row so
+//   that both the staging stores and the MFMA fragment reads are free of bank
+//   conflicts.  The epilogue stages each wave's results through LDS so that
+//   global loads and stores are 16-byte vectors along contiguous columns.
 //
 // Column layout: the tile's BN columns are two halves of BN/2 and every wave
 // owns the same sub-range of BN/4 columns in both halves, so paired epilogues
@@ -87,12 +89,20 @@ __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// Swizzle of the 16-byte unit index within an LDS row of U units.  Rows are
+// read 16 at a time at one unit (MFMA fragments) and written U units at a
+// time per row (staging); the mask is a bijection on the row bits that decide
+// the bank group under both 128-byte and 256-byte LDS access phases.
+template <int U> __device__ __forceinline__ int lds_swz(int r);
+template <> __device__ __forceinline__ int lds_swz<4>(int r) { return (((r >> 1) ^ (r >> 3)) & 1) | ((r >> 1) & 2); }
+template <> __device__ __forceinline__ int lds_swz<8>(int r) { return ((r ^ (r >> 3)) & 1) | (r & 6); }
+
 // LDS arena: two operand stages, reused after the k loop for the epilogue
-// staging (4 waves x 32 rows x (BN/2 + 4) floats).
+// staging (4 waves x 32 rows x (BN/2 + 8) floats).
 template <int BM, int BN, int BK, class CT>
 constexpr int gemm_lds_bytes() {
-  const int ops = 2 * (BM + BN) * (BK + 16 / (int)sizeof(CT)) * (int)sizeof(CT);
-  const int stg = 4 * 32 * (BN / 2 + 4) * 4 + 2 * BM * 4;   // staging + REFINE row info
+  const int ops = 2 * (BM + BN) * BK * (int)sizeof(CT);
+  const int stg = 4 * 32 * (BN / 2 + 8) * 4 + 2 * BM * 4;   // staging + REFINE row info
   return ops > stg ? ops : stg;
 }
 
@@ -101,8 +111,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   typedef Mma<CT> MM;
   typedef typename MM::frag frag;
   constexpr int E = MM::E;
-  constexpr int PAD = 16 / sizeof(CT);
-  constexpr int LR = BK + PAD;                 // LDS row stride (elements)
+  constexpr int LR = BK;                      // LDS row stride (elements), unpadded
   constexpr int TM = BM / 64, TN = BN / 64;    // 32x32 tiles per wave
   constexpr int KV = BK / E;                   // 16-byte vectors per tile row
   constexpr int AV = BM * KV / 256, BV = BN * KV / 256;
@@ -111,7 +120,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   static_assert(TN % 2 == 0, "BN must allow two column halves per wave");
   // epilogue staging (per wave: 32 rows x TN*32 columns of fp32) must fit the arena
   constexpr int WC = TN * 32;
-  constexpr int SLD = WC + 4;                  // staging row stride (floats)
+  constexpr int SLD = WC + 8;                  // staging row stride (floats): rows r and r+4 on disjoint banks
   static_assert(4 * 32 * SLD * 4 <= gemm_lds_bytes<BM, BN, BK, CT>(), "staging does not fit");
   static_assert(WC == BN / 2, "wave column count");
 
@@ -184,33 +193,33 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   }
 
   const TA* Alo = g.A2 ? (const TA*)g.A2 + b1 * g.sA1 + b2 * g.sA2 : nullptr;
+  // per-thread staging slots, fixed for the whole k loop: tile row of each
+  // 16-byte vector, its global row offset (-1: past the end) and its k offset
+  const int kk = (tid % KV) * E;
+  long aoff[AV];
+#pragma unroll
+  for (int i = 0; i < AV; ++i) {
+    const long gr = grow((tid + i * 256) / KV);
+    aoff[i] = gr >= 0 ? gr * g.lda : -1;
+  }
   auto load_stage = [&](int k0, const TA* Ap) {
+    const int gk = k0 + kk;
+    const bool kin = gk < K;
 #pragma unroll
-    for (int i = 0; i < AV; ++i) {
-      const int v = tid + i * 256, r = v / KV, kk = (v % KV) * E;
-      const long gr = grow(r);
-      const int gk = k0 + kk;
-      ra[i] = (gr >= 0 && gk < K) ? VecLoad<CT, TA>::load(Ap + gr * g.lda + gk) : zero_frag<CT>();
-    }
+    for (int i = 0; i < AV; ++i)
+      ra[i] = (aoff[i] >= 0 && kin) ? VecLoad<CT, TA>::load(Ap + aoff[i] + gk) : zero_frag<CT>();
+    const int gkb = (g.bwrap && gk >= g.bwrap) ? gk - g.bwrap : gk;
 #pragma unroll
-    for (int i = 0; i < BV; ++i) {
-      const int v = tid + i * 256, kk = (v % KV) * E;
-      const int gk = k0 + kk;
-      const int gkb = (g.bwrap && gk >= g.bwrap) ? gk - g.bwrap : gk;
-      rb[i] = (bvalid[i] && gk < K) ? VecLoad<CT, TB>::load(brow_ptr[i] + gkb) : zero_frag<CT>();
-    }
+    for (int i = 0; i < BV; ++i) rb[i] = (bvalid[i] && kin) ? VecLoad<CT, TB>::load(brow_ptr[i] + gkb) : zero_frag<CT>();
   };
+  // LDS element offset of (row, 16-byte unit) in a stage
+  auto lds_at = [&](int r, int u) { return r * LR + ((u ^ lds_swz<KV>(r)) * E); };
+  const int su = tid % KV;
   auto store_stage = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < AV; ++i) {
-      const int v = tid + i * 256, r = v / KV, kk = (v % KV) * E;
-      *(frag*)&As[buf * BM * LR + r * LR + kk] = ra[i];
-    }
+    for (int i = 0; i < AV; ++i) *(frag*)&As[buf * BM * LR + lds_at((tid + i * 256) / KV, su)] = ra[i];
 #pragma unroll
-    for (int i = 0; i < BV; ++i) {
-      const int v = tid + i * 256, r = v / KV, kk = (v % KV) * E;
-      *(frag*)&Bs[buf * BN * LR + r * LR + kk] = rb[i];
-    }
+    for (int i = 0; i < BV; ++i) *(frag*)&Bs[buf * BN * LR + lds_at((tid + i * 256) / KV, su)] = rb[i];
   };
 
   // local LDS column of the wave's tile tn (two halves, same sub-range in each)
@@ -244,10 +253,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       frag af[TM], bfr[TN];
 #pragma unroll
       for (int a = 0; a < TM; ++a)
-        af[a] = *(const frag*)&Ac[(wm * (BM / 2) + a * 32 + l32) * LR + ks * 2 * E + lg * E];
+        af[a] = *(const frag*)&Ac[lds_at(wm * (BM / 2) + a * 32 + l32, ks * 2 + lg)];
 #pragma unroll
       for (int b = 0; b < TN; ++b)
-        bfr[b] = *(const frag*)&Bc[(col_base(b) + l32) * LR + ks * 2 * E + lg * E];
+        bfr[b] = *(const frag*)&Bc[lds_at(col_base(b) + l32, ks * 2 + lg)];
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
@@ -277,12 +286,6 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     else if constexpr (EPI == EPI_SWIGLU) return (long)P0 + x;
     else return (long)nt * BN + q * (BN / 2) + wn * (BN / 4) + x;
   };
-
-  float ss[TM][16], dd[TM][16];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) ss[a][j] = dd[a][j] = 0.f;
 
   const int* ridx = (EPI == EPI_REFINE) ? g.ridx + b1 * g.sI1 + b2 * g.sI2 : nullptr;
   const int* crow = (EPI == EPI_REFINE && g.crow) ? g.crow + b1 * g.sI1 + b2 * g.sI2 : nullptr;
@@ -336,128 +339,179 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
           const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
           stg[rl * SLD + b * 32 + l32] = silu_f(acc[a][b][j]) * acc[a][b + TN / 2][j];
         }
-    } else {   // PAIR, REFINE
+    } else {   // PAIR, REFINE: biased pair members; rotation in the vector pass
 #pragma unroll
       for (int b = 0; b < TN / 2; ++b) {
         const int x = b * 32 + l32;                 // position in the wave's run
-        const int jp = pj0 + x;
         const bool pv = P0 + x < N;
-        const int col0 = pc * g.hd + jp, col1 = col0 + hh;
+        const int col0 = pc * g.hd + pj0 + x;
         const float bv0 = (bias && pv) ? to_f32(bias[col0]) : 0.f;
-        const float bv1 = (bias && pv) ? to_f32(bias[col1]) : 0.f;
+        const float bv1 = (bias && pv) ? to_f32(bias[col0 + hh]) : 0.f;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
-          const long r = grow(lbase + rl);
-          const float v0 = acc[a][b][j] + bv0, v1 = acc[a][b + TN / 2][j] + bv1;
-          float y0 = v0, y1 = v1;
-          if (g.tab && pv && r >= 0) {
-            long trow;
-            if constexpr (EPI == EPI_REFINE) {
-              trow = rkey[lbase + rl];
-            } else {
-              trow = r % g.tab_mod;
-            }
-            const float2 cs = g.tab[trow * hh + jp];
-            y0 = v0 * cs.x - v1 * cs.y;
-            y1 = v1 * cs.x + v0 * cs.y;
-          }
-          if (pv) ss[a][j] += v0 * v0 + v1 * v1;
-          if constexpr (EPI == EPI_REFINE) {
-            if (pv && r >= 0) {
-              const float* qe = g.qex + b1 * g.sE1 + b2 * g.sE2 + (long)(rslot[lbase + rl] / g.R) * g.ldqex;
-              dd[a][j] += y0 * qe[col0] + y1 * qe[col1];
-            }
-          } else {
-            stg[rl * SLD + b * 32 + l32] = y0;
-            stg[rl * SLD + (b + TN / 2) * 32 + l32] = y1;
-          }
-        }
-      }
-    }
-    if constexpr (EPI == EPI_REFINE) continue;
-    wave_lds_fence();
-    // ---- 2. staged slice -> global, 16-byte vectors along each run
-    constexpr int NRUN = (EPI == EPI_SWIGLU) ? 1 : 2;
-    constexpr int VE = Vec16<TC>::n;
-    constexpr int VPR = RUN / VE;                  // vectors per run row
-    const bool vec_ok = (g.ldc % VE) == 0 && (((uintptr_t)C & 15) == 0);
-    for (int e = lane; e < 32 * NRUN * VPR; e += 64) {
-      const int rl = e / (NRUN * VPR);
-      const int rem = e - rl * NRUN * VPR;
-      const int q = rem / VPR, vx = (rem - q * VPR) * VE;
-      const long r = grow(lbase + rl);
-      if (r < 0) continue;
-      const float* src = stg + rl * SLD + q * RUN + vx;
-      const long col = run_col(q, vx);
-      TC* dst = C + r * g.ldc + col;
-      int nvalid;
-      if constexpr (PAIRED) {
-        nvalid = N - (P0 + vx);
-      } else {
-        nvalid = N - (int)col;
-      }
-      if (nvalid >= VE && vec_ok) {
-        if constexpr (EPI == EPI_RESID) {
-          f32x4 o = *(const f32x4*)dst;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) o[u] += src[u];
-          *(f32x4*)dst = o;
-        } else {
-          TC tmp[VE];
-#pragma unroll
-          for (int u = 0; u < VE; ++u) tmp[u] = from_f32<TC>(src[u]);
-          *(uint4*)dst = *(const uint4*)tmp;
-        }
-      } else {
-        for (int u = 0; u < VE && u < nvalid; ++u) {
-          if constexpr (EPI == EPI_RESID) dst[u] = from_f32<TC>(to_f32(dst[u]) + src[u]);
-          else dst[u] = from_f32<TC>(src[u]);
-        }
-      }
-      if constexpr (EPI == EPI_PAIR) {
-        if (g.C2) {
-          float* d2 = g.C2 + r * g.ldc + col;
-          if (nvalid >= VE && vec_ok && (((uintptr_t)g.C2 & 15) == 0)) {
-#pragma unroll
-            for (int u = 0; u < VE; u += 4) *(f32x4*)(d2 + u) = *(const f32x4*)(src + u);
-          } else {
-            for (int u = 0; u < VE && u < nvalid; ++u) d2[u] = src[u];
-          }
+          stg[rl * SLD + b * 32 + l32] = acc[a][b][j] + bv0;
+          stg[rl * SLD + (b + TN / 2) * 32 + l32] = acc[a][b + TN / 2][j] + bv1;
         }
       }
     }
     wave_lds_fence();
-  }
-
-  if constexpr (EPI == EPI_PAIR || EPI == EPI_REFINE) {
-    const bool want = (EPI == EPI_PAIR) ? (g.part != nullptr) : true;
-    if (want) {
-      // the wave's pairs lie inside one head c (hd/2 is a multiple of BN/2)
+    if constexpr (EPI == EPI_PAIR || EPI == EPI_REFINE) {
+      // ---- 2p. pairs: 8 pairs per lane and step, rows split over NV lanes.
+      // Rotation by the table row, 16-byte stores of both members, the
+      // row's sum of squares (rotation keeps it) and, for REFINE, the dot
+      // product with the query row; both reduced over the NV lanes of a row.
+      constexpr int PV = 8, NV = RUN / PV;
+      static_assert(NV >= 1 && 64 % NV == 0 && (32 * NV) % 64 == 0, "pair vector pass");
+      const bool want_ss = (EPI == EPI_REFINE) || g.part != nullptr;
       const int nparts = (hh / (BN / 2)) * 2;
       const int pidx = (pj0 / (BN / 2)) * 2 + wn;
 #pragma unroll
-      for (int a = 0; a < TM; ++a)
+      for (int it = 0; it < 32 * NV / 64; ++it) {
+        const int e = lane + 64 * it;
+        const int rl = e / NV, vx = (e % NV) * PV;
+        const long r = grow(lbase + rl);
+        const int nvalid = N - (P0 + vx);
+        float sp = 0.f, dp = 0.f;
+        if (r >= 0 && nvalid > 0) {
+          float v0[PV], v1[PV];
+          const float* s0 = stg + rl * SLD + vx;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          float s = ss[a][j], q = dd[a][j];
+          for (int u = 0; u < PV; u += 4) {
+            const f32x4 a0 = *(const f32x4*)(s0 + u);
+            const f32x4 a1 = *(const f32x4*)(s0 + RUN + u);
 #pragma unroll
-          for (int o = 1; o < 32; o <<= 1) {
-            s += __shfl_xor(s, o);
-            if constexpr (EPI == EPI_REFINE) q += __shfl_xor(q, o);
+            for (int w = 0; w < 4; ++w) {
+              v0[u + w] = a0[w];
+              v1[u + w] = a1[w];
+            }
           }
-          const long r = grow(wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3));
-          if (l32 == 0 && r >= 0) {
-            if constexpr (EPI == EPI_REFINE) {
-              float2* rp = g.rpart + b1 * g.sR1 + b2 * g.sR2;
-              rp[(long)rslot[wm * (BM / 2) + a * 32 + 8 * (j >> 2) + 4 * lg + (j & 3)] * nparts + pidx] =
-                  make_float2(q, s);
+#pragma unroll
+          for (int u = 0; u < PV; ++u) sp += v0[u] * v0[u] + v1[u] * v1[u];
+          const int jp = pj0 + vx;
+          if (g.tab) {
+            long trow;
+            if constexpr (EPI == EPI_REFINE) trow = rkey[lbase + rl];
+            else trow = r % g.tab_mod;
+            const float2* tp = g.tab + trow * hh + jp;
+#pragma unroll
+            for (int u = 0; u < PV; u += 2) {
+              const f32x4 cs = *(const f32x4*)(tp + u);
+              const float y00 = v0[u] * cs[0] - v1[u] * cs[1], y10 = v1[u] * cs[0] + v0[u] * cs[1];
+              const float y01 = v0[u + 1] * cs[2] - v1[u + 1] * cs[3], y11 = v1[u + 1] * cs[2] + v0[u + 1] * cs[3];
+              v0[u] = y00;
+              v1[u] = y10;
+              v0[u + 1] = y01;
+              v1[u + 1] = y11;
+            }
+          }
+          const long col0 = (long)pc * g.hd + jp;
+          if constexpr (EPI == EPI_REFINE) {
+            const float* qe = g.qex + b1 * g.sE1 + b2 * g.sE2 + (long)(rslot[lbase + rl] / g.R) * g.ldqex + col0;
+#pragma unroll
+            for (int u = 0; u < PV; u += 4) {
+              const f32x4 q0 = *(const f32x4*)(qe + u);
+              const f32x4 q1 = *(const f32x4*)(qe + hh + u);
+#pragma unroll
+              for (int w = 0; w < 4; ++w) dp += v0[u + w] * q0[w] + v1[u + w] * q1[w];
+            }
+          } else {
+            TC* d0 = C + r * g.ldc + col0;
+            constexpr int VE = Vec16<TC>::n;
+            const bool vec_ok = nvalid >= PV && (g.ldc % VE) == 0 && (((uintptr_t)C & 15) == 0);
+            if (vec_ok) {
+#pragma unroll
+              for (int u = 0; u < PV; u += VE) {
+                TC t0[VE], t1[VE];
+#pragma unroll
+                for (int w = 0; w < VE; ++w) {
+                  t0[w] = from_f32<TC>(v0[u + w]);
+                  t1[w] = from_f32<TC>(v1[u + w]);
+                }
+                *(uint4*)(d0 + u) = *(const uint4*)t0;
+                *(uint4*)(d0 + hh + u) = *(const uint4*)t1;
+              }
             } else {
-              g.part[r * g.ldpart + pc * nparts + pidx] = s;
+              for (int u = 0; u < PV && u < nvalid; ++u) {
+                d0[u] = from_f32<TC>(v0[u]);
+                d0[hh + u] = from_f32<TC>(v1[u]);
+              }
+            }
+            if (g.C2) {
+              float* e0 = g.C2 + r * g.ldc + col0;
+              if (vec_ok && (((uintptr_t)g.C2 & 15) == 0)) {
+#pragma unroll
+                for (int u = 0; u < PV; u += 4) {
+                  *(f32x4*)(e0 + u) = f32x4{v0[u], v0[u + 1], v0[u + 2], v0[u + 3]};
+                  *(f32x4*)(e0 + hh + u) = f32x4{v1[u], v1[u + 1], v1[u + 2], v1[u + 3]};
+                }
+              } else {
+                for (int u = 0; u < PV && u < nvalid; ++u) {
+                  e0[u] = v0[u];
+                  e0[hh + u] = v1[u];
+                }
+              }
             }
           }
         }
+        if (want_ss) {
+#pragma unroll
+          for (int o = 1; o < NV; o <<= 1) {
+            sp += __shfl_xor(sp, o);
+            if constexpr (EPI == EPI_REFINE) dp += __shfl_xor(dp, o);
+          }
+          if ((e % NV) == 0 && r >= 0) {
+            if constexpr (EPI == EPI_REFINE) {
+              float2* rp = g.rpart + b1 * g.sR1 + b2 * g.sR2;
+              rp[(long)rslot[lbase + rl] * nparts + pidx] = make_float2(dp, sp);
+            } else {
+              g.part[r * g.ldpart + pc * nparts + pidx] = sp;
+            }
+          }
+        }
+      }
+    } else {
+      // ---- 2. staged slice -> global, 16-byte vectors along each run
+      constexpr int NRUN = (EPI == EPI_SWIGLU) ? 1 : 2;
+      constexpr int VE = Vec16<TC>::n;
+      constexpr int VPR = RUN / VE;                  // vectors per run row
+      const bool vec_ok = (g.ldc % VE) == 0 && (((uintptr_t)C & 15) == 0);
+      for (int e = lane; e < 32 * NRUN * VPR; e += 64) {
+        const int rl = e / (NRUN * VPR);
+        const int rem = e - rl * NRUN * VPR;
+        const int q = rem / VPR, vx = (rem - q * VPR) * VE;
+        const long r = grow(lbase + rl);
+        if (r < 0) continue;
+        const float* src = stg + rl * SLD + q * RUN + vx;
+        const long col = run_col(q, vx);
+        TC* dst = C + r * g.ldc + col;
+        int nvalid;
+        if constexpr (PAIRED) {
+          nvalid = N - (P0 + vx);
+        } else {
+          nvalid = N - (int)col;
+        }
+        if (nvalid >= VE && vec_ok) {
+          if constexpr (EPI == EPI_RESID) {
+            f32x4 o = *(const f32x4*)dst;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) o[u] += src[u];
+            *(f32x4*)dst = o;
+          } else {
+            TC tmp[VE];
+#pragma unroll
+            for (int u = 0; u < VE; ++u) tmp[u] = from_f32<TC>(src[u]);
+            *(uint4*)dst = *(const uint4*)tmp;
+          }
+        } else {
+          for (int u = 0; u < VE && u < nvalid; ++u) {
+            if constexpr (EPI == EPI_RESID) dst[u] = from_f32<TC>(to_f32(dst[u]) + src[u]);
+            else dst[u] = from_f32<TC>(src[u]);
+          }
+        }
+      }
     }
+    wave_lds_fence();
   }
 }
 

@@ -453,4 +453,24 @@ __global__ void zero_cols_kernel(T* __restrict__ A, long rows, int ld, int c0, i
   }
 }
 
+// Element-type conversion of up to CONV_SEGS weight matrices per launch
+// (bf16 -> fp16 for the MFMA operands), one segment per grid row, 8 elements
+// per thread and step; segment lengths are multiples of 8 and 16-byte aligned.
+constexpr int CONV_SEGS = 16;
+struct ConvSegs {
+  const void* src[CONV_SEGS];
+  void* dst[CONV_SEGS];
+  long n8[CONV_SEGS];   // length / 8
+};
+
+template <class IT, class CT>
+__global__ void convert_kernel(ConvSegs segs) {
+  const int s = blockIdx.y;
+  const IT* src = (const IT*)segs.src[s];
+  CT* dst = (CT*)segs.dst[s];
+  const long n8 = segs.n8[s];
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n8; i += (long)gridDim.x * blockDim.x)
+    *(typename Mma<CT>::frag*)(dst + 8 * i) = VecLoad<CT, IT>::load(src + 8 * i);
+}
+
 }  // namespace still

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "../../include/still.h"
@@ -130,6 +131,7 @@ struct Dims {
 
 struct Plan {
   size_t pq, tab_ck, tab_cq, tab_bk, tab_bq;
+  size_t wconv;          // bf16 mode: the layer's weight matrices converted to fp16
   size_t X, XT, Z, Y, q, partq, rq, O;
   size_t Ylo, qex, cval, cidx, ridx, rval, Xc, rpart, crow, ccount;   // logit refinement
   // union region: cross-attention key side ...
@@ -203,7 +205,50 @@ static still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims*
   return STILL_OK;
 }
 
-static Plan make_plan(const Dims& m) {
+// The weight matrices of one layer in a fixed order, with their element
+// counts: per block the cross-attention (if the block has it), self-attention
+// and FFN matrices, then the two output heads.  `f` is called as
+// f(src, elements, slot) with slot the matrix's address in a still_block_weights
+// / still_layer_weights copy whose pointer is to be replaced.
+template <class F>
+static void for_each_matrix(const still_config* c, const Dims& m, const still_layer_weights* w,
+                            still_block_weights* blocks, const void** wkey, const void** wval, F f) {
+  for (int b = 0; b < c->n_blocks; ++b) {
+    const still_block_weights* bw = w ? &w->blocks[b] : nullptr;
+    still_block_weights* o = blocks ? &blocks[b] : nullptr;
+    auto put = [&](const void* const* src, long n, const void** slot) { f(src ? *src : nullptr, n, slot); };
+#define MAT(name, n) put(bw ? &bw->name : nullptr, (long)(n), o ? &o->name : nullptr)
+    if (c->cross_every_block || b == 0) {
+      MAT(ca_wq, (long)m.Ec * m.D);
+      MAT(ca_wk, (long)m.Ec * m.d2);
+      MAT(ca_wv, (long)m.Ec * m.d2);
+      MAT(ca_wo, (long)m.D * m.Ec);
+    }
+    if (m.ns > 0) {
+      MAT(sa_wq, (long)m.Es * m.D);
+      MAT(sa_wk, (long)m.Es * m.D);
+      MAT(sa_wv, (long)m.Es * m.D);
+      MAT(sa_wo, (long)m.D * m.Es);
+    }
+    if (c->ffn_kind == STILL_FFN_SWIGLU) MAT(ffn_wg, (long)m.F * m.D);
+    if (c->ffn_kind != STILL_FFN_NONE) {
+      MAT(ffn_wu, (long)m.F * m.D);
+      MAT(ffn_wd, (long)m.D * m.F);
+    }
+#undef MAT
+  }
+  f(w ? w->w_key : nullptr, (long)m.d * m.D, wkey);
+  f(w ? w->w_val : nullptr, (long)m.d * m.D, wval);
+}
+
+static long matrix_elems(const still_config* c, const Dims& m) {
+  long total = 0;
+  for_each_matrix(c, m, nullptr, nullptr, nullptr, nullptr,
+                  [&](const void*, long n, const void**) { total += rup(n, 128); });
+  return total;
+}
+
+static Plan make_plan(const still_config* c, const Dims& m) {
   Plan p;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -219,6 +264,7 @@ static Plan make_plan(const Dims& m) {
   p.tab_cq = take(8ul * m.t * (m.dc / 2));
   p.tab_bk = take(8ul * m.N * (m.d / 2));
   p.tab_bq = take(8ul * m.t * (m.d / 2));
+  p.wconv = m.fp32 ? 0 : take(2ul * matrix_elems(c, m));
   p.X = take(cs * HN * m.d2);
   p.XT = take(cs * (size_t)m.H * m.d2 * m.Npad);
   p.Z = take(4ul * Ht * m.D);
@@ -368,6 +414,42 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
   const float2* tab_bq = (const float2*)(ws + p.tab_bq);
   const float LOG2E = 1.4426950408889634f;
 
+  // bf16 mode: the layer's weight matrices converted once to the fp16 MFMA
+  // operand type (biases and latents stay bf16); every GEMM then reads fp16.
+  std::vector<still_block_weights> cblocks(w->blocks, w->blocks + cfg->n_blocks);
+  still_layer_weights cw = *w;
+  if constexpr (!std::is_same<IT, CT>::value) {
+    CT* dst = (CT*)(ws + p.wconv);
+    ConvSegs segs;
+    memset(&segs, 0, sizeof segs);
+    int ns = 0;
+    long longest = 0;
+    hipError_t err = hipSuccess;
+    auto flush = [&]() {
+      if (ns == 0 || err != hipSuccess) return;
+      TIMED(STILL_K_OTHER);
+      hipLaunchKernelGGL((convert_kernel<IT, CT>), dim3(grid1d(longest) > 1024 ? 1024 : grid1d(longest), ns),
+                         dim3(256), 0, st, segs);
+      err = hipGetLastError();
+      memset(&segs, 0, sizeof segs);
+      ns = 0;
+      longest = 0;
+    };
+    for_each_matrix(cfg, m, w, cblocks.data(), &cw.w_key, &cw.w_val, [&](const void* src, long n, const void** slot) {
+      segs.src[ns] = src;
+      segs.dst[ns] = dst;
+      segs.n8[ns] = n / 8;
+      if (n / 8 > longest) longest = n / 8;
+      *slot = dst;
+      dst += rup(n, 128);
+      if (++ns == CONV_SEGS) flush();
+    });
+    flush();
+    HIP_TRY(err);
+    cw.blocks = cblocks.data();
+    w = &cw;
+  }
+
   // RoPE-fix staging of X = [R(-p) K ; V] and X^T
   {
     int RW = 64;
@@ -425,7 +507,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.tab_mod = m.t;
         g.part = partq;
         g.ldpart = (long)m.nc * m.np_c;
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_QPROJ)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_QPROJ)));
       }
       {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
         GemmArgs g = gargs((int)HN, m.Ec / 2, m.d2, X, m.d2, bw.ca_wk, m.d2, k, m.Ec);
@@ -439,7 +521,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.tab_mod = (int)m.N;
         g.part = partk;
         g.ldpart = (long)m.nc * m.np_c;
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_KPROJ)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_KPROJ)));
       }
       HIP_TRY(finalize(partq, Ht, m.nc, m.np_c, rq));
       HIP_TRY(finalize(partk, HN, m.nc, m.np_c, rk));
@@ -527,7 +609,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
             g.rpart = (float2*)(ws + p.rpart);
             g.sR1 = (long)m.nc * m.t * m.R * (m.dc / 64);
             g.sR2 = (long)m.t * m.R * (m.dc / 64);
-            HIP_TRY((gemm<CT, CT, IT, float, IT, EPI_REFINE>(g, m.H * m.nc, st, STILL_K_REFINE)));
+            HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_REFINE>(g, m.H * m.nc, st, STILL_K_REFINE)));
           }
           ra.R = m.R;
           ra.NP = m.dc / 64;
@@ -551,11 +633,11 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.sA2 = m.d2;
         g.sB2 = (long)m.dc * m.d2;
         g.sC2 = m.dc;
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_STORE>(g, m.nc, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE>(g, m.nc, st)));
       }
       {  // Z += Concat(heads) W_O^T
         GemmArgs g = gargs((int)Ht, m.D, m.Ec, head, m.Ec, bw.ca_wo, m.Ec, Z, m.D);
-        HIP_TRY((gemm<CT, CT, IT, float, IT, EPI_RESID>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID>(g, 1, st)));
       }
     }
     // ---------------- latent self-attention: Z += SelfAttn(RMSNorm(Z))
@@ -577,18 +659,18 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.hd = m.ds;
         g.part = partqs;
         g.ldpart = (long)m.ns * m.np_s;
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
         g.B = bw.sa_wk;
         g.bias = bw.sa_bk;
         g.C = ks;
         g.part = partks;
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_PAIR>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
       }
       {  // v^T[h] = W_V^sa Y[h]^T : [Es][tpad] per KV head
         GemmArgs g = gargs(m.Es, m.t, m.D, bw.sa_wv, m.D, Y, m.D, vT, m.tpad);
         g.sB1 = (long)m.t * m.D;
         g.sC1 = (long)m.Es * m.tpad;
-        HIP_TRY((gemm<CT, IT, CT, CT, IT, EPI_STORE>(g, m.H, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE>(g, m.H, st)));
         if (m.tpad > m.t) {
           TIMED(STILL_K_OTHER);
           hipLaunchKernelGGL((zero_cols_kernel<CT>), dim3(grid1d((long)m.H * m.Es * (m.tpad - m.t))), dim3(256), 0,
@@ -650,7 +732,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
       }
       {
         GemmArgs g = gargs((int)Ht, m.D, m.Es, Osa, m.Es, bw.sa_wo, m.Es, Z, m.D);
-        HIP_TRY((gemm<CT, CT, IT, float, IT, EPI_RESID>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID>(g, 1, st)));
       }
     }
     // ---------------- FFN: Z += FFN(RMSNorm(Z))
@@ -660,13 +742,13 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
       if (cfg->ffn_kind == STILL_FFN_SWIGLU) {
         GemmArgs g = gargs((int)Ht, m.F, m.D, Y, m.D, bw.ffn_wg, m.D, hid, m.F);
         g.B2 = bw.ffn_wu;
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_SWIGLU>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_SWIGLU>(g, 1, st)));
       } else {
         GemmArgs g = gargs((int)Ht, m.F, m.D, Y, m.D, bw.ffn_wu, m.D, hid, m.F);
-        HIP_TRY((gemm<CT, CT, IT, CT, IT, EPI_GELU>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_GELU>(g, 1, st)));
       }
       GemmArgs g = gargs((int)Ht, m.D, m.F, hid, m.F, bw.ffn_wd, m.F, Z, m.D);
-      HIP_TRY((gemm<CT, CT, IT, float, IT, EPI_RESID>(g, 1, st)));
+      HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID>(g, 1, st)));
     }
   }
   // ---------------- output heads: C_k = Z_out W_key^T (re-rotated), C_v = Z_out W_val^T
@@ -680,11 +762,11 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
       HIP_TRY(rmsnorm());
       gk.A = Y;
       gv.A = Y;
-      HIP_TRY((gemm<CT, CT, IT, IT, IT, EPI_PAIR>(gk, 1, st)));
-      HIP_TRY((gemm<CT, CT, IT, IT, IT, EPI_STORE>(gv, 1, st)));
+      HIP_TRY((gemm<CT, CT, CT, IT, IT, EPI_PAIR>(gk, 1, st)));
+      HIP_TRY((gemm<CT, CT, CT, IT, IT, EPI_STORE>(gv, 1, st)));
     } else {
-      HIP_TRY((gemm<CT, float, IT, IT, IT, EPI_PAIR>(gk, 1, st)));
-      HIP_TRY((gemm<CT, float, IT, IT, IT, EPI_STORE>(gv, 1, st)));
+      HIP_TRY((gemm<CT, float, CT, IT, IT, EPI_PAIR>(gk, 1, st)));
+      HIP_TRY((gemm<CT, float, CT, IT, IT, EPI_STORE>(gv, 1, st)));
     }
   }
   return STILL_OK;
@@ -758,7 +840,7 @@ static still_status compact(const still_config* cfg, int32_t L, const still_laye
     if (misaligned(K[l]) || misaligned(V[l]) || misaligned(Ck[l]) || misaligned(Cv[l]))
       return fail(STILL_E_INVAL, "layer %d: cache/output pointers must be 16-byte aligned", l);
   }
-  const Plan p = make_plan(m);
+  const Plan p = make_plan(cfg, m);
   if (!workspace) return fail(STILL_E_WORKSPACE, "workspace is NULL");
   if (workspace_bytes < p.total)
     return fail(STILL_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, p.total);
@@ -786,7 +868,7 @@ extern "C" {
 size_t still_workspace_size(const still_config* cfg, int64_t N, int32_t t, int32_t n_layers) {
   Dims m;
   if (n_layers < 1 || make_dims(cfg, N, t, &m) != STILL_OK) return 0;
-  return make_plan(m).total;
+  return make_plan(cfg, m).total;
 }
 
 still_status still_compact_layer(const still_config* cfg, const still_layer_weights* w, const void* K, const void* V,
