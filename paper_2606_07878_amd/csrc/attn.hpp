@@ -275,16 +275,21 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
 namespace still {
 
 // ---------------------------------------------------------------------------
-// fp16 cross-attention, workgroup = TT latents x one key range, 4 waves.
-// Key blocks of 256: wave w owns keys [64w, 64w+64) of the block in the QK
-// product and output features [w*D2/4, (w+1)*D2/4) in the P.X product.
-//   QK:  S^T[key][lat] over the head width in chunks of DK.  K fragments are
-//        loaded from global memory straight into registers (each key row is
-//        read once per workgroup); Q chunks are staged through LDS and shared
-//        by the 4 waves.  Within a chunk, lane half g holds the contiguous run
-//        [g*DK/2, (g+1)*DK/2) of the head width, so MFMA step s pairs element
-//        e of both operands with width index g*DK/2 + 8s + e (any fixed
-//        pairing contracts every index once).
+// fp16 cross-attention, workgroup = TT latents x one key range, NW waves.
+// Key blocks of 256: wave w owns keys [w*256/NW, (w+1)*256/NW) of the block
+// in the QK product and output features [w*D2/NW, (w+1)*D2/NW) in the P.X
+// product (8 waves keep each wave's accumulators small enough for two waves
+// per SIMD).
+//   QK:  S^T[key][lat] over the head width.  Q is staged through LDS in
+//        chunks of QC (one barrier per chunk) and shared by the waves.  K
+//        fragments go from global memory straight into registers (each key
+//        row is read once per workgroup) in groups of 32 of the head width,
+//        through a ring of QC/32 groups: the group used now is reloaded with
+//        the same group of the next chunk, so every K load has a whole chunk
+//        of MFMA work to arrive.  Within a group, lane half g holds the
+//        contiguous run [16g, 16g + 16), so MFMA step s pairs element e of
+//        both operands with width index 16g + 8s + e (any fixed pairing
+//        contracts every index once).
 //   softmax: per-latent block maxima combined across the waves through LDS;
 //        P (fp16) written to LDS as [latent][key].
 //   P.X: O^T[feat][lat] += X^T[feat][key] P^T[key][lat]; X^T fragments from
@@ -293,21 +298,26 @@ namespace still {
 // are consecutive workgroups of one XCD: they read the same keys through
 // that XCD's L2.
 // ---------------------------------------------------------------------------
-template <int TT, int DK, int D2, int TOPK>
-__global__ __launch_bounds__(256) void xattn_f16_kernel(AttnArgs a) {
+template <int TT, int QC, int D2, int TOPK, int NW>
+__global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
   constexpr int LT = TT / 32;            // latent tiles
   constexpr int KB = 256;                // keys per block
-  constexpr int FW = D2 / 4;             // output features per wave
+  constexpr int NT = 64 * NW;            // threads
+  constexpr int KW = KB / NW;            // keys per wave (QK)
+  constexpr int KT = KW / 32;            // key tiles per wave
+  constexpr int FW = D2 / NW;            // output features per wave
   constexpr int FT = FW / 32;            // feature tiles per wave
-  constexpr int NS = DK / 16;            // MFMA steps per chunk
-  constexpr int LQ = DK + 8;             // Q stage row stride (halfs)
+  constexpr int NBK = 2 * NW;            // top-key buckets per latent (wave, lane half)
+  constexpr int G = 32;                  // head-width group of one K load (2 MFMA steps)
+  constexpr int NG = QC / G;             // groups per Q chunk = depth of the K ring
+  constexpr int LQ = QC + 8;             // Q stage row stride (halfs)
   constexpr int LP = KB + 8;             // P row stride (halfs)
-  constexpr int QV = TT * DK / 8 / 256;  // Q stage vectors per thread
-  static_assert(FT >= 1 && QV >= 1 && NS >= 1, "tile sizes");
+  constexpr int QV = TT * QC / 8 / NT;   // Q stage vectors per thread
+  static_assert(FT >= 1 && KT >= 1 && QV >= 1 && NG >= 1 && (TT * QC / 8) % NT == 0, "tile sizes");
 
   __shared__ __attribute__((aligned(16))) f16 Qs[2][TT * LQ];
   __shared__ __attribute__((aligned(16))) f16 Ps[TT * LP];
-  __shared__ float red_m[4][TT], red_l[4][TT];
+  __shared__ float red_m[NW][TT], red_l[NW][TT];
   __shared__ float rks[KB];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -342,21 +352,32 @@ __global__ __launch_bounds__(256) void xattn_f16_kernel(AttnArgs a) {
   for (int f = 0; f < FT; ++f)
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) o[f][lt] = zero16();
-  float tv[LT][TOPK > 0 ? TOPK : 1];
-  int ti[LT][TOPK > 0 ? TOPK : 1];
+  // Candidate keys for the logit refinement: each lane keeps, per latent
+  // tile, a sorted list of its TOPK largest logits (bucket = wave, lane half)
+  // in the output arrays cval/cidx (only the lane itself touches its list),
+  // and in a register the list's smallest entry.  Keys below the running
+  // maximum minus REFINE_MARGIN can never be selected and are skipped, which
+  // makes list updates rare.
+  float th[LT];
 #pragma unroll
-  for (int lt = 0; lt < LT; ++lt)
+  for (int lt = 0; lt < LT; ++lt) {
+    th[lt] = -INFINITY;
+    const int lat = t0 + 32 * lt + l32;
+    if (TOPK > 0 && lat < a.t) {
+      const long row = ((long)split * HC + hc) * a.t + lat;
 #pragma unroll
-    for (int q = 0; q < (TOPK > 0 ? TOPK : 1); ++q) {
-      tv[lt][q] = -INFINITY;
-      ti[lt][q] = -1;
+      for (int q = 0; q < (TOPK > 0 ? TOPK : 1); ++q) {
+        a.cval[row * (NBK * TOPK) + (2 * w + lg) * TOPK + q] = -INFINITY;
+        a.cidx[row * (NBK * TOPK) + (2 * w + lg) * TOPK + q] = -1;
+      }
     }
+  }
 
   half8 qreg[QV];
   auto load_q = [&](int d0) {
 #pragma unroll
     for (int i = 0; i < QV; ++i) {
-      const int v = tid + i * 256, r = v / (DK / 8), kk = (v % (DK / 8)) * 8;
+      const int v = tid + i * NT, r = v / (QC / 8), kk = (v % (QC / 8)) * 8;
       const int lat = t0 + r;
       qreg[i] = lat < a.t ? *(const half8*)(qb + (long)lat * a.ldq + d0 + kk) : zero_frag<f16>();
     }
@@ -364,18 +385,18 @@ __global__ __launch_bounds__(256) void xattn_f16_kernel(AttnArgs a) {
   auto store_q = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < QV; ++i) {
-      const int v = tid + i * 256, r = v / (DK / 8), kk = (v % (DK / 8)) * 8;
+      const int v = tid + i * NT, r = v / (QC / 8), kk = (v % (QC / 8)) * 8;
       *(half8*)&Qs[buf][r * LQ + kk] = qreg[i];
     }
   };
-  // K fragments of this wave's 64 keys for one chunk: [key tile][step]
-  auto load_k = [&](half8 (&kr)[2][NS], int n0, int d0) {
+  // K fragments of this wave's keys for one group of 32: [key tile][step]
+  auto load_kg = [&](half8 (&kr)[KT][2], int n0, int d0) {
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      const int n = n0 + 64 * w + 32 * kt + l32;
-      const f16* src = kb + (long)n * a.ldk + d0 + (DK / 2) * lg;
+    for (int kt = 0; kt < KT; ++kt) {
+      const int n = n0 + KW * w + 32 * kt + l32;
+      const f16* src = kb + (long)n * a.ldk + d0 + 16 * lg;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) kr[kt][s] = n < nend ? *(const half8*)(src + 8 * s) : zero_frag<f16>();
+      for (int s = 0; s < 2; ++s) kr[kt][s] = n < nend ? *(const half8*)(src + 8 * s) : zero_frag<f16>();
     }
   };
   // X^T fragments for P.X step group s4: [feature tile][step]
@@ -389,88 +410,72 @@ __global__ __launch_bounds__(256) void xattn_f16_kernel(AttnArgs a) {
     }
   };
 
-  const int nd = a.dc / DK;   // even (checked on the host)
-  half8 kA[2][NS], kB[2][NS];
+  const int nch = a.dc / QC;   // a.dc is a multiple of QC (checked on the host)
+  half8 kr[NG][KT][2];
   half8 xA[FT][4], xB[FT][4];
   for (int n0 = nbeg; n0 < nend; n0 += KB) {
-    f32x16 s[LT][2];
+    f32x16 s[LT][KT];
 #pragma unroll
-    for (int lt = 0; lt < LT; ++lt) s[lt][0] = s[lt][1] = zero16();
+    for (int lt = 0; lt < LT; ++lt)
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) s[lt][kt] = zero16();
     load_q(0);
-    load_k(kA, n0, 0);
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) load_kg(kr[gi], n0, gi * G);
     store_q(0);
-    {
-      const int n = n0 + tid;
-      rks[tid] = n < nend ? rkb[(long)n * a.nc] : 0.f;
+    for (int i = tid; i < KB; i += NT) {
+      const int n = n0 + i;
+      rks[i] = n < nend ? rkb[(long)n * a.nc] : 0.f;
     }
     __syncthreads();
-    auto chunk = [&](int ci, half8 (&kc)[2][NS], half8 (&kn)[2][NS]) {
-      const int cur = ci & 1;
-      const bool more = ci + 1 < nd;
-      if (more) {
-        load_q((ci + 1) * DK);
-        load_k(kn, n0, (ci + 1) * DK);
-      } else {
-        load_x(xA, n0, 0);
-      }
+    for (int c = 0; c < nch; ++c) {
+      const int cur = c & 1;
+      const bool more = c + 1 < nch;
+      if (more) load_q((c + 1) * QC);
+      else load_x(xA, n0, 0);
 #pragma unroll
-      for (int st = 0; st < NS; ++st) {
+      for (int gi = 0; gi < NG; ++gi) {
 #pragma unroll
-        for (int lt = 0; lt < LT; ++lt) {
-          const half8 bq = *(const half8*)&Qs[cur][(32 * lt + l32) * LQ + (DK / 2) * lg + 8 * st];
+        for (int st = 0; st < 2; ++st) {
 #pragma unroll
-          for (int kt = 0; kt < 2; ++kt)
-            s[lt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kc[kt][st], bq, s[lt][kt], 0, 0, 0);
+          for (int lt = 0; lt < LT; ++lt) {
+            const half8 bq = *(const half8*)&Qs[cur][(32 * lt + l32) * LQ + gi * G + 16 * lg + 8 * st];
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt)
+              s[lt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[gi][kt][st], bq, s[lt][kt], 0, 0, 0);
+          }
         }
+        if (more) load_kg(kr[gi], n0, (c + 1) * QC + gi * G);
       }
       if (more) store_q(cur ^ 1);
       __syncthreads();
-    };
-    for (int ci = 0; ci < nd; ci += 2) {
-      chunk(ci, kA, kB);
-      chunk(ci + 1, kB, kA);
     }
 
     // ---- softmax statistics for the block
-    float rkv[2][16];
+    float rkv[KT][16];
     const bool tail = n0 + KB > nend;    // keys past the range only in a split's last block
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const int kl = 64 * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
+        const int kl = KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
         rkv[kt][j] = (tail && n0 + kl >= nend) ? -INFINITY : rks[kl];
       }
-    float mx[LT];
+    float mx[LT], lmx[LT];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
       mx[lt] = -INFINITY;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const int kl = 64 * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
+          const int kl = KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
           float x = s[lt][kt][j] * rkv[kt][j];   // masked keys carry rk = -inf (S may be 0)
           x = (rkv[kt][j] == -INFINITY) ? -INFINITY : x;
           s[lt][kt][j] = x;
           mx[lt] = fmaxf(mx[lt], x);
-          if constexpr (TOPK > 0) {
-            if (x > tv[lt][TOPK - 1]) {
-              float v = x;
-              int id = n0 + kl;
-#pragma unroll
-              for (int q = 0; q < TOPK; ++q) {
-                const bool gt = v > tv[lt][q];
-                const float tq = tv[lt][q];
-                const int iq = ti[lt][q];
-                tv[lt][q] = gt ? v : tq;
-                ti[lt][q] = gt ? id : iq;
-                v = gt ? tq : v;
-                id = gt ? iq : id;
-              }
-            }
-          }
         }
+      lmx[lt] = mx[lt];
       mx[lt] = fmaxf(mx[lt], __shfl_xor(mx[lt], 32));
       if (lg == 0) red_m[w][32 * lt + l32] = mx[lt];
     }
@@ -479,12 +484,14 @@ __global__ __launch_bounds__(256) void xattn_f16_kernel(AttnArgs a) {
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
       const int li = 32 * lt + l32;
-      const float mb = fmaxf(fmaxf(red_m[0][li], red_m[1][li]), fmaxf(red_m[2][li], red_m[3][li]));
+      float mb = red_m[0][li];
+#pragma unroll
+      for (int u = 1; u < NW; ++u) mb = fmaxf(mb, red_m[u][li]);
       const float m_new = fmaxf(m_run[lt], mb);
       alpha[lt] = (m_new == -INFINITY) ? 1.f : exp2f(m_run[lt] - m_new);
       float ps = 0.f;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
         for (int jq = 0; jq < 4; ++jq) {
           half4 pv;
@@ -494,10 +501,50 @@ __global__ __launch_bounds__(256) void xattn_f16_kernel(AttnArgs a) {
             ps += p;
             pv[u] = (f16)p;
           }
-          *(half4*)&Ps[li * LP + 64 * w + 32 * kt + 8 * jq + 4 * lg] = pv;
+          *(half4*)&Ps[li * LP + KW * w + 32 * kt + 8 * jq + 4 * lg] = pv;
         }
       ps += __shfl_xor(ps, 32);
       if (lg == 0) red_l[w][li] = ps;
+      if constexpr (TOPK > 0) {
+        const float cut0 = m_new - REFINE_MARGIN;
+        if (lmx[lt] > fmaxf(th[lt], cut0) && t0 + li < a.t) {   // rare: update this lane's list
+          const long row = ((long)split * HC + hc) * a.t + t0 + li;
+          float* cv = a.cval + row * (NBK * TOPK) + (2 * w + lg) * TOPK;
+          int* ci = a.cidx + row * (NBK * TOPK) + (2 * w + lg) * TOPK;
+          float tv[TOPK > 0 ? TOPK : 1];
+          int ti[TOPK > 0 ? TOPK : 1];
+#pragma unroll
+          for (int q = 0; q < TOPK; ++q) {
+            tv[q] = cv[q];
+            ti[q] = ci[q];
+          }
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+              float v = s[lt][kt][j];
+              if (v > fmaxf(tv[TOPK - 1], cut0)) {
+                int id = n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
+#pragma unroll
+                for (int q = 0; q < TOPK; ++q) {
+                  const bool gt = v > tv[q];
+                  const float tq = tv[q];
+                  const int iq = ti[q];
+                  tv[q] = gt ? v : tq;
+                  ti[q] = gt ? id : iq;
+                  v = gt ? tq : v;
+                  id = gt ? iq : id;
+                }
+              }
+            }
+#pragma unroll
+          for (int q = 0; q < TOPK; ++q) {
+            cv[q] = tv[q];
+            ci[q] = ti[q];
+          }
+          th[lt] = tv[TOPK - 1];
+        }
+      }
       m_run[lt] = m_new;
       // rescale only when some latent of the tile saw a new maximum
       if (__any(alpha[lt] != 1.f)) {
@@ -511,7 +558,10 @@ __global__ __launch_bounds__(256) void xattn_f16_kernel(AttnArgs a) {
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
       const int li = 32 * lt + l32;
-      l_run[lt] = l_run[lt] * alpha[lt] + (red_l[0][li] + red_l[1][li]) + (red_l[2][li] + red_l[3][li]);
+      float lb = 0.f;
+#pragma unroll
+      for (int u = 0; u < NW; ++u) lb += red_l[u][li];
+      l_run[lt] = l_run[lt] * alpha[lt] + lb;
     }
 
     // ---- O^T += X^T P^T over the block's 256 keys
@@ -548,13 +598,6 @@ __global__ __launch_bounds__(256) void xattn_f16_kernel(AttnArgs a) {
     if (w == 0 && lg == 0) {
       a.mpart[row] = m_run[lt];
       a.lpart[row] = l_run[lt];
-    }
-    if constexpr (TOPK > 0) {
-#pragma unroll
-      for (int q = 0; q < TOPK; ++q) {
-        a.cval[row * (8 * TOPK) + (2 * w + lg) * TOPK + q] = tv[lt][q];
-        a.cidx[row * (8 * TOPK) + (2 * w + lg) * TOPK + q] = ti[lt][q];
-      }
     }
   }
 }

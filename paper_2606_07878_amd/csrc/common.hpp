@@ -106,6 +106,10 @@ template <> struct VecLoad<float, float> {
   static __device__ __forceinline__ f32x4 load(const float* p) { return *(const f32x4*)p; }
 };
 
+// Keys whose fp16-path logit lies within this many log2 units of their row's
+// maximum are candidates for the exact-logit refinement of cross-attention.
+constexpr float REFINE_MARGIN = 10.f;
+
 template <class CT> __device__ __forceinline__ typename Mma<CT>::frag zero_frag() {
   typename Mma<CT>::frag z;
 #pragma unroll

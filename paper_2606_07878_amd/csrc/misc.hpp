@@ -272,7 +272,6 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* __restri
 // selected keys is exact for them; every other key keeps a weight below
 // 2^-REFINE_MARGIN of the row maximum.
 // ---------------------------------------------------------------------------
-constexpr float REFINE_MARGIN = 10.f;   // log2 units
 
 // Pick, per latent row, the R largest fp16 logits among the flash pass's
 // per-split candidates that lie within REFINE_MARGIN of the row maximum.

@@ -112,6 +112,8 @@ constexpr int ATT_TOPK = 4;    // keys tracked per latent half-lane for logit re
 constexpr int XATT_KB = 256;   // keys per block of the fp16 cross-attention kernel
 constexpr int XATT_TOPK = 4;   // keys tracked per (latent, wave, lane half) by the fp16 kernel
 constexpr int REFINE_R = 4;    // keys per latent whose logits are recomputed accurately
+// waves of the fp16 cross-attention workgroup for a value width d2 = 2d
+constexpr int xatt_waves(int d2) { return d2 >= 256 ? 8 : 4; }
 
 // ---------------------------------------------------------------------------
 // Derived dimensions and workspace layout
@@ -196,7 +198,7 @@ static still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims*
   m->np_c = m->dc / GEMM_BN * 2;
   m->np_s = m->ns > 0 ? m->ds / GEMM_BN * 2 : 0;
   m->topk = m->fp32 ? ATT_TOPK : XATT_TOPK;
-  m->ncand = m->fp32 ? 2 * ATT_TOPK : 8 * XATT_TOPK;
+  m->ncand = m->fp32 ? 2 * ATT_TOPK : 2 * xatt_waves(m->d2) * XATT_TOPK;
   m->R = REFINE_R;
   m->att_tt = (m->fp32 || m->d2 <= 256) ? 128 : 64;
   m->splits = choose_splits(*m);
@@ -321,9 +323,16 @@ template <class CT> struct Tile;
 template <> struct Tile<f16> { static constexpr int BM = 128, BN = GEMM_BN, BK = 32; };
 template <> struct Tile<float> { static constexpr int BM = 128, BN = GEMM_BN, BK = 16; };
 
+// Long reductions take twice the k depth per stage (half the barriers and
+// twice the MFMA work between operand loads); short ones keep BK so that more
+// workgroups fit a CU.
+constexpr int GEMM_LONG_K = 512;
+
 template <class CT, class TA, class TB, class TC, class TBias, int EPI>
 static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st, int cls = STILL_K_LATENT) {
   timing::Scope ts(cls, st);
+  if (g.K >= GEMM_LONG_K)
+    return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
   return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
 }
 
@@ -356,9 +365,10 @@ static hipError_t launch_attn(const AttnArgs& a, int splits, hipStream_t st) {
   if constexpr (sizeof(CT) == 2) {
     constexpr int TT = D2 <= 256 ? 128 : 64;
     const int ntt = (a.t + TT - 1) / TT;
-    constexpr int DK = D2 == 256 ? 32 : 64;   // register budget (no scratch spills)
-    hipLaunchKernelGGL((xattn_f16_kernel<TT, DK, D2, XATT_TOPK>), dim3(ntt * a.H * a.nc * splits), dim3(256), 0, st,
-                       a);
+    constexpr int NW = xatt_waves(D2);
+    constexpr int QC = NW == 8 ? 128 : 64;    // head width per Q stage (register budget of the K ring)
+    hipLaunchKernelGGL((xattn_f16_kernel<TT, QC, D2, XATT_TOPK, NW>), dim3(ntt * a.H * a.nc * splits), dim3(64 * NW),
+                       0, st, a);
   } else {
     hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, (D2 > 256 ? 32 : ATT_NB), 32, D2, ATT_TOPK>), grid, dim3(256),
                        0, st, a);
