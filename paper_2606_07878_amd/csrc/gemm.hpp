@@ -132,19 +132,31 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   const int wm = wave >> 1, wn = wave & 1;
   const int l32 = lane & 31, lg = lane >> 5;
 
-  // Tile order: each XCD takes a contiguous range of tiles (workgroup ids are
-  // dealt to the 8 XCDs round robin), walked in groups of 8 M tiles x all N
-  // tiles, so the operand tiles the XCD's concurrent workgroups touch stay in
-  // its L2.
+  // Tile order.  Workgroup ids are dealt to the 8 XCDs round robin; XCD x
+  // takes the M tiles congruent to x mod 8 (so that rows cut short by a
+  // device-side row count leave every XCD the same share of work) and walks
+  // them in groups of 8 M tiles x all N tiles, so that the operand tiles its
+  // concurrent workgroups touch stay in its L2.
   const int gx = gridDim.x, gy = gridDim.y;
   int lin = blockIdx.x + gx * blockIdx.y;
-  const int T = gx * gy;
-  if ((T & 7) == 0) lin = (lin & 7) * (T >> 3) + (lin >> 3);
   constexpr int GM = 8;
-  const int grp = lin / (GM * gx), gm0 = grp * GM;
-  const int gsz = min(GM, gy - gm0);
-  const int inl = lin - grp * GM * gx;
-  const int mt = gm0 + inl % gsz, nt = inl / gsz;
+  int mt, nt;
+  if ((gy & 7) == 0) {
+    const int xcd = lin & 7, i = lin >> 3, gyx = gy >> 3;
+    const int grp = i / (GM * gx), gm0 = grp * GM;
+    const int gsz = min(GM, gyx - gm0);
+    const int inl = i - grp * GM * gx;
+    mt = (gm0 + inl % gsz) * 8 + xcd;
+    nt = inl / gsz;
+  } else {
+    const int T = gx * gy;
+    if ((T & 7) == 0) lin = (lin & 7) * (T >> 3) + (lin >> 3);
+    const int grp = lin / (GM * gx), gm0 = grp * GM;
+    const int gsz = min(GM, gy - gm0);
+    const int inl = lin - grp * GM * gx;
+    mt = gm0 + inl % gsz;
+    nt = inl / gsz;
+  }
 
   const int bz = blockIdx.z, b1 = bz / g.nb2, b2 = bz - b1 * g.nb2;
   const int M = g.mcount ? g.mcount[bz] : g.M;
@@ -168,8 +180,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     return rr < Mg ? (long)grp * g.mgstride + rr : -1;
   };
 
-  // global -> register staging
-  frag ra[AV], rb[BV];
+  // global -> register staging, two sets: loads run two k steps ahead
+  frag ra[2][AV], rb[2][BV];
   const TB* brow_ptr[BV];
   bool bvalid[BV];
 #pragma unroll
@@ -190,9 +202,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       bvalid[i] = n < N;
       brow_ptr[i] = B + (long)n * g.ldb;
     }
+    if (!bvalid[i]) brow_ptr[i] = B;   // loads always issue (from row 0) and are zeroed
   }
 
   const TA* Alo = g.A2 ? (const TA*)g.A2 + b1 * g.sA1 + b2 * g.sA2 : nullptr;
+  const int nk1 = (K + BK - 1) / BK;
+  const int nk = Alo ? 2 * nk1 : nk1;      // split A: second pass over K with the low part
   // per-thread staging slots, fixed for the whole k loop: tile row of each
   // 16-byte vector, its global row offset (-1: past the end) and its k offset
   const int kk = (tid % KV) * E;
@@ -202,24 +217,34 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     const long gr = grow((tid + i * 256) / KV);
     aoff[i] = gr >= 0 ? gr * g.lda : -1;
   }
-  auto load_stage = [&](int k0, const TA* Ap) {
-    const int gk = k0 + kk;
+  // Loads of k step kn into a register set.  Every load instruction issues
+  // (out-of-range rows and k read row 0 / column 0) and the zeroing of those
+  // happens only when the set is stored to LDS, so the number of loads in
+  // flight is static and the wait before a stage store leaves the following
+  // step's loads outstanding.  Returns whether this thread's k run is in range.
+  auto load_stage = [&](int kn, frag (&xa)[AV], frag (&xb)[BV]) -> bool {
+    const bool lo = kn >= nk1;                 // split A: second pass with the low part
+    const TA* Ap = lo ? Alo : A;
+    const int gk = (lo ? kn - nk1 : kn) * BK + kk;
     const bool kin = gk < K;
+    const int gks = kin ? gk : 0;
 #pragma unroll
-    for (int i = 0; i < AV; ++i)
-      ra[i] = (aoff[i] >= 0 && kin) ? VecLoad<CT, TA>::load(Ap + aoff[i] + gk) : zero_frag<CT>();
-    const int gkb = (g.bwrap && gk >= g.bwrap) ? gk - g.bwrap : gk;
+    for (int i = 0; i < AV; ++i) xa[i] = VecLoad<CT, TA>::load(Ap + (aoff[i] >= 0 ? aoff[i] : 0) + gks);
+    const int gkb = (g.bwrap && gks >= g.bwrap) ? gks - g.bwrap : gks;
 #pragma unroll
-    for (int i = 0; i < BV; ++i) rb[i] = (bvalid[i] && kin) ? VecLoad<CT, TB>::load(brow_ptr[i] + gkb) : zero_frag<CT>();
+    for (int i = 0; i < BV; ++i) xb[i] = VecLoad<CT, TB>::load(brow_ptr[i] + gkb);
+    return kin;
   };
   // LDS element offset of (row, 16-byte unit) in a stage
   auto lds_at = [&](int r, int u) { return r * LR + ((u ^ lds_swz<KV>(r)) * E); };
   const int su = tid % KV;
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](int buf, const frag (&xa)[AV], const frag (&xb)[BV], bool kin) {
 #pragma unroll
-    for (int i = 0; i < AV; ++i) *(frag*)&As[buf * BM * LR + lds_at((tid + i * 256) / KV, su)] = ra[i];
+    for (int i = 0; i < AV; ++i)
+      *(frag*)&As[buf * BM * LR + lds_at((tid + i * 256) / KV, su)] = (aoff[i] >= 0 && kin) ? xa[i] : zero_frag<CT>();
 #pragma unroll
-    for (int i = 0; i < BV; ++i) *(frag*)&Bs[buf * BN * LR + lds_at((tid + i * 256) / KV, su)] = rb[i];
+    for (int i = 0; i < BV; ++i)
+      *(frag*)&Bs[buf * BN * LR + lds_at((tid + i * 256) / KV, su)] = (bvalid[i] && kin) ? xb[i] : zero_frag<CT>();
   };
 
   // local LDS column of the wave's tile tn (two halves, same sub-range in each)
@@ -234,20 +259,13 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int b = 0; b < TN; ++b) acc[a][b] = zero16();
 
-  const int nk1 = (K + BK - 1) / BK;
-  const int nk = Alo ? 2 * nk1 : nk1;      // split A: second pass over K with the low part
-  load_stage(0, A);
-  store_stage(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      const int kn = kt + 1;
-      if (kn < nk1) load_stage(kn * BK, A);
-      else load_stage((kn - nk1) * BK, Alo);
-    }
-    const CT* Ac = As + cur * BM * LR;
-    const CT* Bc = Bs + cur * BN * LR;
+  // k steps past the end reload the last one (their data is never stored)
+  auto issue = [&](int kn, frag (&xa)[AV], frag (&xb)[BV]) -> bool {
+    return load_stage(kn < nk ? kn : nk - 1, xa, xb);
+  };
+  auto compute = [&](int buf) {
+    const CT* Ac = As + buf * BM * LR;
+    const CT* Bc = Bs + buf * BN * LR;
 #pragma unroll
     for (int ks = 0; ks < BK / (2 * E); ++ks) {
       frag af[TM], bfr[TN];
@@ -262,9 +280,27 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
         for (int b = 0; b < TN; ++b) MM::mma(acc[a][b], af[a], bfr[b]);
     }
-    if (kt + 1 < nk) store_stage(cur ^ 1);
+  };
+  // step kt: LDS stage kt & 1 holds k step kt, register set nxt holds k step
+  // kt + 1 (in flight); set cur (already in LDS) takes k step kt + 2.
+  bool kin0, kin1;
+  auto step = [&](int kt, frag (&ca)[AV], frag (&cb)[BV], bool& ckin, frag (&na)[AV], frag (&nb)[BV], bool nkin) {
+    ckin = issue(kt + 2, ca, cb);
+    __builtin_amdgcn_sched_barrier(0);   // loads go out before this step's MFMA work
+    compute(kt & 1);
+    if (kt + 1 < nk) store_stage((kt + 1) & 1, na, nb, nkin);
     __syncthreads();
+  };
+  kin0 = issue(0, ra[0], rb[0]);
+  store_stage(0, ra[0], rb[0], kin0);
+  kin1 = issue(1, ra[1], rb[1]);
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {   // both steps unconditional: one loop state at the back edge
+    step(kt, ra[0], rb[0], kin0, ra[1], rb[1], kin1);
+    step(kt + 1, ra[1], rb[1], kin1, ra[0], rb[0], kin0);
   }
+  if (kt < nk) step(kt, ra[0], rb[0], kin0, ra[1], rb[1], kin1);
 
   // ------------------------------------------------------------------ epilogue
   // Per 32-row slice a of the wave's block: values -> LDS staging (fp32, the

@@ -200,6 +200,41 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* __restri
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
   const float* s = S + row * ld;
+  if (!ref.q && ld <= 1024) {
+    // the whole row in registers: element 256u + 4*lane + e of the row
+    float v[16];
+    float m = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i0 = 256 * u + 4 * lane;
+      f32x4 x = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+      if (i0 < ld) x = *(const f32x4*)(s + i0);   // ld is a multiple of 4
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        v[4 * u + e] = (i0 + e < t) ? x[e] : -INFINITY;
+        m = fmaxf(m, v[4 * u + e]);
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      v[k] = expf(v[k] - m);   // masked entries give 0
+      sum += v[k];
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+    const float inv = 1.f / sum;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i0 = 256 * u + 4 * lane;
+      if (i0 >= ld) continue;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) P[row * ld + i0 + e] = from_f32<CT>(v[4 * u + e] * inv);
+    }
+    return;
+  }
   float m = -INFINITY;
   for (int i = lane; i < t; i += 64) m = fmaxf(m, s[i]);
 #pragma unroll
@@ -392,53 +427,74 @@ struct RefineArgs {
   float scale_log2, l2_eps;
 };
 
-template <class CT>
+// One wave per output row (h, c, i); lane l owns features [l*VPL, (l+1)*VPL).
+template <class CT, int VPL>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ opart, const float* __restrict__ mpart,
                                                     const float* __restrict__ lpart, int S, int H, int nc, int t,
-                                                    int d2, CT* __restrict__ O, RefineArgs ra) {
-  __shared__ float sdelta[8];
-  const long row = blockIdx.x;     // (h*nc + c)*t + i
+                                                    CT* __restrict__ O, RefineArgs ra) {
+  constexpr int d2 = 64 * VPL;
+  const int lane = threadIdx.x & 63;
+  const long row = blockIdx.x * 4L + (threadIdx.x >> 6);   // (h*nc + c)*t + i
   const long HCT = (long)H * nc * t;
+  if (row >= HCT) return;   // whole wave
   const int hc = (int)(row / t), i = (int)(row - (long)hc * t);
   const int h = hc / nc, c = hc - h * nc;
   float M = -INFINITY;
-  for (int s = 0; s < S; ++s) M = fmaxf(M, mpart[s * HCT + row]);
+  for (int s = lane; s < S; s += 64) M = fmaxf(M, mpart[s * HCT + row]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
   float L = 0.f;
-  for (int s = 0; s < S; ++s) {
+  for (int s = lane; s < S; s += 64) {
     const float ms = mpart[s * HCT + row];
     if (ms != -INFINITY) L += exp2f(ms - M) * lpart[s * HCT + row];
   }
-  if ((int)threadIdx.x < ra.R) {
-    const int r = threadIdx.x;
-    float dl = 0.f;
-    if (ra.ridx[row * ra.R + r] >= 0) {
-      const float2* p = ra.rpart + (row * ra.R + r) * ra.NP;
+  // weight change of each refined key: 2^(exact - M) - 2^(fp16 - M)
+  float dl = 0.f;
+  int key = -1;
+  if (lane < ra.R) {
+    key = ra.ridx[row * ra.R + lane];
+    if (key >= 0) {
+      const float2* p = ra.rpart + (row * ra.R + lane) * ra.NP;
       float dot = 0.f, ss = 0.f;
       for (int k = 0; k < ra.NP; ++k) {
         dot += p[k].x;
         ss += p[k].y;
       }
       const float sx = ra.scale_log2 * ra.rq[((long)h * t + i) * nc + c] * dot / fmaxf(sqrtf(ss), ra.l2_eps);
-      dl = exp2f(sx - M) - exp2f(ra.rval[row * ra.R + r] - M);
+      dl = exp2f(sx - M) - exp2f(ra.rval[row * ra.R + lane] - M);
     }
-    sdelta[r] = dl;
   }
-  __syncthreads();
-  for (int r = 0; r < ra.R; ++r) L += sdelta[r];
+  L += dl;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
+  const int f0 = lane * VPL;
+  float acc[VPL];
+#pragma unroll
+  for (int u = 0; u < VPL; ++u) acc[u] = 0.f;
+  for (int s = 0; s < S; ++s) {
+    const float ms = mpart[s * HCT + row];
+    if (ms == -INFINITY) continue;
+    const float ws = exp2f(ms - M);
+    const float* op = opart + (s * HCT + row) * d2 + f0;
+#pragma unroll
+    for (int u = 0; u < VPL; u += 2) {
+      const float2 v = *(const float2*)(op + u);
+      acc[u] += ws * v.x;
+      acc[u + 1] += ws * v.y;
+    }
+  }
+  for (int r = 0; r < ra.R; ++r) {
+    const int n = __shfl(key, r);
+    const float dr = __shfl(dl, r);
+    if (n < 0) continue;
+    const CT* x = (const CT*)ra.X + ((long)h * ra.N + n) * d2 + f0;
+#pragma unroll
+    for (int u = 0; u < VPL; ++u) acc[u] += dr * to_f32(x[u]);
+  }
   const float invL = 1.f / L;
-  CT* dst = O + ((long)h * t + i) * ((long)nc * d2) + (long)c * d2;
-  for (int f = threadIdx.x; f < d2; f += 256) {
-    float acc = 0.f;
-    for (int s = 0; s < S; ++s) {
-      const float ms = mpart[s * HCT + row];
-      if (ms != -INFINITY) acc += exp2f(ms - M) * opart[(s * HCT + row) * d2 + f];
-    }
-    for (int r = 0; r < ra.R; ++r) {
-      const int n = ra.ridx[row * ra.R + r];
-      if (n >= 0) acc += sdelta[r] * to_f32(((const CT*)ra.X)[((long)h * ra.N + n) * d2 + f]);
-    }
-    dst[f] = from_f32<CT>(acc * invL);
-  }
+  CT* dst = O + ((long)h * t + i) * ((long)nc * d2) + (long)c * d2 + f0;
+#pragma unroll
+  for (int u = 0; u < VPL; ++u) dst[u] = from_f32<CT>(acc[u] * invL);
 }
 
 // Fill columns [c0, c1) of a [rows][ld] matrix with zeros.

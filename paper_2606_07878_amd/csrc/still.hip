@@ -633,8 +633,16 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
           ra.l2_eps = cfg->l2_eps;
         }
         TIMED(STILL_K_OTHER);
-        hipLaunchKernelGGL((merge_kernel<CT>), dim3((unsigned)(Ht * m.nc)), dim3(256), 0, st, a.opart, a.mpart,
-                           a.lpart, m.splits, m.H, m.nc, m.t, m.d2, O, ra);
+        const dim3 mg((unsigned)((Ht * m.nc + 3) / 4));
+        if (m.d2 == 128)
+          hipLaunchKernelGGL((merge_kernel<CT, 2>), mg, dim3(256), 0, st, a.opart, a.mpart, a.lpart, m.splits, m.H,
+                             m.nc, m.t, O, ra);
+        else if (m.d2 == 256)
+          hipLaunchKernelGGL((merge_kernel<CT, 4>), mg, dim3(256), 0, st, a.opart, a.mpart, a.lpart, m.splits, m.H,
+                             m.nc, m.t, O, ra);
+        else
+          hipLaunchKernelGGL((merge_kernel<CT, 8>), mg, dim3(256), 0, st, a.opart, a.mpart, a.lpart, m.splits, m.H,
+                             m.nc, m.t, O, ra);
         HIP_TRY(hipGetLastError());
       }
       {  // head_c = O_c W_V,c^T   (batched over cross heads c)
