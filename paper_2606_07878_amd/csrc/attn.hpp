@@ -317,8 +317,8 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
 
   __shared__ __attribute__((aligned(16))) f16 Qs[2][TT * LQ];
   __shared__ __attribute__((aligned(16))) f16 Ps[TT * LP];
-  __shared__ float red_m[NW][TT], red_l[NW][TT];
-  __shared__ float rks[KB];
+  __shared__ float red_m[TT][NW], red_l[TT][NW];
+  __shared__ float2 rks[KB];   // (1/||k~||, 0) or (0, -inf) past the key range
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, lg = lane >> 5;
@@ -327,8 +327,11 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
   const int total = gridDim.x;
   int L = blockIdx.x;
   if ((total & 7) == 0) L = (L & 7) * (total >> 3) + (L >> 3);
+  // order: latent tile fastest, then split, then (KV head, cross head): the
+  // workgroups an XCD runs at once share one Q tile set and few key ranges
+  const int S = total / (ntt * HC);
   const int tt = L % ntt, rest = L / ntt;
-  const int hc = rest % HC, split = rest / HC;
+  const int split = rest % S, hc = rest / S;
   const int h = hc / a.nc, c = hc - h * a.nc;
   const int t0 = tt * TT;
   const int nbeg = split * a.keys_per_split;
@@ -373,40 +376,51 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
     }
   }
 
+  // Loads address uniform bases (q, k, X^T of this head) with 32-bit element
+  // offsets (the host bounds them), and are branch-free: rows past the end
+  // read the last valid row, whose values are then zeroed (Q) or masked out
+  // of the softmax (K), so the number of loads in flight stays static.
   half8 qreg[QV];
   auto load_q = [&](int d0) {
 #pragma unroll
     for (int i = 0; i < QV; ++i) {
       const int v = tid + i * NT, r = v / (QC / 8), kk = (v % (QC / 8)) * 8;
-      const int lat = t0 + r;
-      qreg[i] = lat < a.t ? *(const half8*)(qb + (long)lat * a.ldq + d0 + kk) : zero_frag<f16>();
+      const unsigned lat = (unsigned)min(t0 + r, a.t - 1);
+      qreg[i] = *(const half8*)(qb + (lat * (unsigned)a.ldq + (unsigned)(d0 + kk)));
     }
   };
   auto store_q = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < QV; ++i) {
       const int v = tid + i * NT, r = v / (QC / 8), kk = (v % (QC / 8)) * 8;
-      *(half8*)&Qs[buf][r * LQ + kk] = qreg[i];
+      *(half8*)&Qs[buf][r * LQ + kk] = (t0 + r < a.t) ? qreg[i] : zero_frag<f16>();
     }
   };
   // K fragments of this wave's keys for one group of 32: [key tile][step]
-  auto load_kg = [&](half8 (&kr)[KT][2], int n0, int d0) {
+  unsigned krow[KT];
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) krow[kt] = 0;
+  auto set_krows = [&](int n0) {
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt) {
-      const int n = n0 + KW * w + 32 * kt + l32;
-      const f16* src = kb + (long)n * a.ldk + d0 + 16 * lg;
-#pragma unroll
-      for (int s = 0; s < 2; ++s) kr[kt][s] = n < nend ? *(const half8*)(src + 8 * s) : zero_frag<f16>();
+      const unsigned n = (unsigned)min(n0 + KW * w + 32 * kt + l32, nend - 1);
+      krow[kt] = n * (unsigned)a.ldk + 16u * lg;
     }
+  };
+  auto load_kg = [&](half8 (&kr)[KT][2], int d0) {
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+      for (int s = 0; s < 2; ++s) kr[kt][s] = *(const half8*)(kb + (krow[kt] + (unsigned)(d0 + 8 * s)));
   };
   // X^T fragments for P.X step group s4: [feature tile][step]
   auto load_x = [&](half8 (&xr)[FT][4], int n0, int s4) {
 #pragma unroll
     for (int f = 0; f < FT; ++f) {
-      const int fr = FW * w + 32 * f + l32;
-      const f16* src = xtb + (long)fr * a.ldxt + n0 + 64 * s4 + 32 * lg;
+      const unsigned fr = FW * w + 32 * f + l32;
+      const unsigned off = fr * (unsigned)a.ldxt + (unsigned)(n0 + 64 * s4 + 32 * lg);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) xr[f][s] = *(const half8*)(src + 8 * s);   // X^T padded to the block size
+      for (int s = 0; s < 4; ++s) xr[f][s] = *(const half8*)(xtb + (off + 8u * s));   // X^T padded to the block size
     }
   };
 
@@ -420,12 +434,13 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) s[lt][kt] = zero16();
     load_q(0);
+    set_krows(n0);
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) load_kg(kr[gi], n0, gi * G);
+    for (int gi = 0; gi < NG; ++gi) load_kg(kr[gi], gi * G);
     store_q(0);
     for (int i = tid; i < KB; i += NT) {
       const int n = n0 + i;
-      rks[i] = n < nend ? rkb[(long)n * a.nc] : 0.f;
+      rks[i] = n < nend ? make_float2(rkb[(long)n * a.nc], 0.f) : make_float2(0.f, -INFINITY);
     }
     __syncthreads();
     for (int c = 0; c < nch; ++c) {
@@ -445,50 +460,49 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
               s[lt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[gi][kt][st], bq, s[lt][kt], 0, 0, 0);
           }
         }
-        if (more) load_kg(kr[gi], n0, (c + 1) * QC + gi * G);
+        if (more) load_kg(kr[gi], (c + 1) * QC + gi * G);
       }
       if (more) store_q(cur ^ 1);
       __syncthreads();
     }
 
-    // ---- softmax statistics for the block
-    float rkv[KT][16];
-    const bool tail = n0 + KB > nend;    // keys past the range only in a split's last block
+    // ---- softmax statistics for the block: logit (log2 units) = S * rk + mask
+    float mx[LT], lmx[LT];
+#pragma unroll
+    for (int lt = 0; lt < LT; ++lt) mx[lt] = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int kl = KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
-        rkv[kt][j] = (tail && n0 + kl >= nend) ? -INFINITY : rks[kl];
+      for (int jq = 0; jq < 4; ++jq) {
+        // keys KW*w + 32*kt + 8*jq + 4*lg + (0..3): two 16-byte LDS reads
+        const float4 r01 = *(const float4*)&rks[KW * w + 32 * kt + 8 * jq + 4 * lg];
+        const float4 r23 = *(const float4*)&rks[KW * w + 32 * kt + 8 * jq + 4 * lg + 2];
+        const float rk[4] = {r01.x, r01.z, r23.x, r23.z}, mk[4] = {r01.y, r01.w, r23.y, r23.w};
+#pragma unroll
+        for (int lt = 0; lt < LT; ++lt) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) s[lt][kt][4 * jq + u] = fmaf(s[lt][kt][4 * jq + u], rk[u], mk[u]);
+          mx[lt] = fmaxf(fmaxf(mx[lt], fmaxf(s[lt][kt][4 * jq], s[lt][kt][4 * jq + 1])),
+                         fmaxf(s[lt][kt][4 * jq + 2], s[lt][kt][4 * jq + 3]));
+        }
       }
-    float mx[LT], lmx[LT];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
-      mx[lt] = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int kl = KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
-          float x = s[lt][kt][j] * rkv[kt][j];   // masked keys carry rk = -inf (S may be 0)
-          x = (rkv[kt][j] == -INFINITY) ? -INFINITY : x;
-          s[lt][kt][j] = x;
-          mx[lt] = fmaxf(mx[lt], x);
-        }
       lmx[lt] = mx[lt];
       mx[lt] = fmaxf(mx[lt], __shfl_xor(mx[lt], 32));
-      if (lg == 0) red_m[w][32 * lt + l32] = mx[lt];
+      if (lg == 0) red_m[32 * lt + l32][w] = mx[lt];
     }
     __syncthreads();
     float alpha[LT];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
       const int li = 32 * lt + l32;
-      float mb = red_m[0][li];
+      float mb = red_m[li][0];
 #pragma unroll
-      for (int u = 1; u < NW; ++u) mb = fmaxf(mb, red_m[u][li]);
+      for (int u = 1; u < NW; ++u) mb = fmaxf(mb, red_m[li][u]);
       const float m_new = fmaxf(m_run[lt], mb);
-      alpha[lt] = (m_new == -INFINITY) ? 1.f : exp2f(m_run[lt] - m_new);
+      const float mref = (m_new == -INFINITY) ? 0.f : m_new;   // all keys masked so far: every p is 0
+      alpha[lt] = __builtin_amdgcn_exp2f(m_run[lt] - mref);   // m_run = -inf -> 0 (o, l are 0 then)
       float ps = 0.f;
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt)
@@ -497,14 +511,14 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
           half4 pv;
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float p = (m_new == -INFINITY) ? 0.f : exp2f(s[lt][kt][4 * jq + u] - m_new);
+            const float p = __builtin_amdgcn_exp2f(s[lt][kt][4 * jq + u] - mref);
             ps += p;
             pv[u] = (f16)p;
           }
           *(half4*)&Ps[li * LP + KW * w + 32 * kt + 8 * jq + 4 * lg] = pv;
         }
       ps += __shfl_xor(ps, 32);
-      if (lg == 0) red_l[w][li] = ps;
+      if (lg == 0) red_l[li][w] = ps;
       if constexpr (TOPK > 0) {
         const float cut0 = m_new - REFINE_MARGIN;
         if (lmx[lt] > fmaxf(th[lt], cut0) && t0 + li < a.t) {   // rare: update this lane's list
@@ -518,9 +532,7 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
             tv[q] = cv[q];
             ti[q] = ci[q];
           }
-#pragma unroll
           for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
             for (int j = 0; j < 16; ++j) {
               float v = s[lt][kt][j];
               if (v > fmaxf(tv[TOPK - 1], cut0)) {
@@ -560,7 +572,7 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
       const int li = 32 * lt + l32;
       float lb = 0.f;
 #pragma unroll
-      for (int u = 0; u < NW; ++u) lb += red_l[u][li];
+      for (int u = 0; u < NW; ++u) lb += red_l[li][u];
       l_run[lt] = l_run[lt] * alpha[lt] + lb;
     }
 

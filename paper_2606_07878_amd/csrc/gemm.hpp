@@ -54,7 +54,7 @@ struct GemmArgs {
   int hd;              // PAIR / REFINE: head width
   const float2* tab;   // rotation table, row (r % tab_mod) (REFINE: row ridx[r]), entry [row*hd/2 + j]; NULL = none
   int tab_mod;
-  float* part;         // PAIR: per-row sum-of-squares partials, NULL = none
+  float* part;         // PAIR: sum-of-squares partials [head*nparts + p][ldpart] (ldpart >= rows), NULL = none
   long ldpart;
   float* C2;           // PAIR: optional fp32 copy of the (rotated) outputs, ldc as C
   // REFINE: row r of batch (b1, b2) is candidate slot r of latent i = r / R;
@@ -501,7 +501,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
               float2* rp = g.rpart + b1 * g.sR1 + b2 * g.sR2;
               rp[(long)rslot[lbase + rl] * nparts + pidx] = make_float2(dp, sp);
             } else {
-              g.part[r * g.ldpart + pc * nparts + pidx] = sp;
+              g.part[(long)(pc * nparts + pidx) * g.ldpart + r] = sp;   // partial-major: rows contiguous
             }
           }
         }

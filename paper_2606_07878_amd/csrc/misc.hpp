@@ -166,14 +166,16 @@ __global__ void qprescale_kernel(f16* __restrict__ q, const float* __restrict__ 
   }
 }
 
-// rn[r][c] = 1 / max(sqrt(sum_p part[r][c][p]), eps)   (QK-norm factors)
+// rn[r][c] = 1 / max(sqrt(sum_p part[c*np + p][r]), eps)   (QK-norm factors)
 __global__ void finalize_norm_kernel(const float* __restrict__ part, long rows, int nh, int np,
                                      float eps, float* __restrict__ rn) {
   const long total = rows * nh;
   for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
-    const float* p = part + i * np;
+    const long r = i / nh;
+    const int c = (int)(i - r * nh);
+    const float* p = part + (long)c * np * rows + r;   // partials [c*np + k][rows]
     float s = 0.f;
-    for (int k = 0; k < np; ++k) s += p[k];
+    for (int k = 0; k < np; ++k) s += p[(long)k * rows];
     rn[i] = 1.f / fmaxf(sqrtf(s), eps);
   }
 }

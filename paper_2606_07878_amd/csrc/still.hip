@@ -191,6 +191,9 @@ static still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims*
     return fail(STILL_E_UNSUPPORTED, "self head width %d must be a multiple of %d", m->ds, GEMM_BN);
   if (m->D % 8) return fail(STILL_E_UNSUPPORTED, "latent_dim %d must be a multiple of 8", m->D);
   if (m->F % 8) return fail(STILL_E_UNSUPPORTED, "ffn_hidden %d must be a multiple of 8", m->F);
+  // the fp16 cross-attention addresses one head's q, k and X^T with 32-bit offsets
+  if ((double)N * m->nc * m->dc * 2.0 >= 4294967296.0 || (double)t * m->nc * m->dc * 2.0 >= 4294967296.0)
+    return fail(STILL_E_UNSUPPORTED, "N or t too large for one head's 4 GiB key/query span");
   if ((long)m->H * N > (long)GEMM_BN * 65535L)
     return fail(STILL_E_UNSUPPORTED, "H*N = %lld exceeds the supported %ld rows", (long long)(m->H * N), (long)GEMM_BN * 65535L);
   m->tpad = (int)rup(t, 64);
@@ -516,7 +519,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.tab = tab_cq;
         g.tab_mod = m.t;
         g.part = partq;
-        g.ldpart = (long)m.nc * m.np_c;
+        g.ldpart = Ht;
         HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_QPROJ)));
       }
       {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
@@ -530,7 +533,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.tab = tab_ck;
         g.tab_mod = (int)m.N;
         g.part = partk;
-        g.ldpart = (long)m.nc * m.np_c;
+        g.ldpart = HN;
         HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_KPROJ)));
       }
       HIP_TRY(finalize(partq, Ht, m.nc, m.np_c, rq));
@@ -676,7 +679,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.bias = bw.sa_bq;
         g.hd = m.ds;
         g.part = partqs;
-        g.ldpart = (long)m.ns * m.np_s;
+        g.ldpart = Ht;
         HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
         g.B = bw.sa_wk;
         g.bias = bw.sa_bk;
