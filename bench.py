@@ -25,6 +25,24 @@ sys.path.insert(0, ROOT)
 PEAK_FP16_TFLOPS = 2500.0     # MI355X dense fp16/bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
+# HBM bytes per launch of the cross-attention kernel on the default workload,
+# from rocprofv3 PMC FETCH_SIZE / WRITE_SIZE passes scaled by what the same
+# counters read for a 1 GiB device copy (factors 2.0 and 1.0).  Valid only for
+# the kernel sources with this digest; any later change reports null.
+MEASURED_TRAFFIC = {"workload": 2, "sources_sha256_16": "3eca465a0f624b36", "bytes_per_launch": 6543332812}
+KERNEL_SOURCES = ("paper_2606_07878_amd/csrc/attn.hpp", "paper_2606_07878_amd/csrc/common.hpp")
+
+
+def measured_traffic(workload_id: int):
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if workload_id != MEASURED_TRAFFIC["workload"] or h.hexdigest()[:16] != MEASURED_TRAFFIC["sources_sha256_16"]:
+        return None
+    return MEASURED_TRAFFIC["bytes_per_launch"]
+
 
 def ca_flops_per_launch(w) -> float:
     c = w.cfg
@@ -194,7 +212,9 @@ def main():
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "mfma", "kernel": "cross_attn", "achieved": round(achieved, 2),
                      "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP16_TFLOPS, 4),
-                     "traffic": None, "avg_launch_ms": round(avg_att_s * 1e3, 4), "launches": att_n,
+                     "traffic": measured_traffic(args.workload), "traffic_unit": "bytes/launch",
+                     "avg_launch_ms": round(avg_att_s * 1e3, 4),
+                     "launches": att_n,
                      "flops_per_launch": ca_flops_per_launch(w)},
         "layer_mfma_frac": round(layer_flops(w) / (ms_step / L / 1e3) / 1e12 / PEAK_FP16_TFLOPS, 4),
         "kernel_ms_per_layer": breakdown,
