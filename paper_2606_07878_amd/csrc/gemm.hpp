@@ -140,13 +140,13 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   const int gx = gridDim.x, gy = gridDim.y;
   int lin = blockIdx.x + gx * blockIdx.y;
   constexpr int GM = 8;
-  int mt, nt;
+  int mt0, nt;
   if ((gy & 7) == 0) {
     const int xcd = lin & 7, i = lin >> 3, gyx = gy >> 3;
     const int grp = i / (GM * gx), gm0 = grp * GM;
     const int gsz = min(GM, gyx - gm0);
     const int inl = i - grp * GM * gx;
-    mt = (gm0 + inl % gsz) * 8 + xcd;
+    mt0 = (gm0 + inl % gsz) * 8 + xcd;
     nt = inl / gsz;
   } else {
     const int T = gx * gy;
@@ -154,13 +154,17 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     const int grp = lin / (GM * gx), gm0 = grp * GM;
     const int gsz = min(GM, gy - gm0);
     const int inl = lin - grp * GM * gx;
-    mt = gm0 + inl % gsz;
+    mt0 = gm0 + inl % gsz;
     nt = inl / gsz;
   }
 
   const int bz = blockIdx.z, b1 = bz / g.nb2, b2 = bz - b1 * g.nb2;
   const int M = g.mcount ? g.mcount[bz] : g.M;
-  if (mt * BM >= M) return;   // whole workgroup past the (device-side) row count
+  // REFINE with a device-side row count: the grid holds fewer M tiles than
+  // the row bound and each workgroup walks M tiles mt0, mt0 + gridDim.y, ...
+  // (no launches of workgroups that would find no rows).  Other kernels take
+  // one tile per workgroup (and exit at once past a device-side row count).
+  for (int mt = mt0; (long)mt * BM < M; mt += gy) {
   const TA* A = (const TA*)g.A + b1 * g.sA1 + b2 * g.sA2;
   const TB* B = (const TB*)g.B + b1 * g.sB1 + b2 * g.sB2;
   const TB* B2 = PAIRED && g.B2 ? (const TB*)g.B2 + b1 * g.sB1 + b2 * g.sB2 : nullptr;
@@ -549,6 +553,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     }
     wave_lds_fence();
   }
+  if constexpr (EPI != EPI_REFINE) break;   // one tile per workgroup
+  if (!g.mcount) break;
+  __syncthreads();        // LDS (staging, row info) is reused by the next tile
+  }  // M tile loop
 }
 
 template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK>
@@ -556,7 +564,8 @@ hipError_t launch_gemm(const GemmArgs& g, int batch, hipStream_t st) {
   constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
   const int ntn = PAIRED ? (g.N + BN / 2 - 1) / (BN / 2) : (g.N + BN - 1) / BN;
   const int mg = g.mgroups > 1 ? g.mgroups : 1;
-  const int ntm = mg == 1 ? (g.M + BM - 1) / BM : (g.M / mg + BM / mg - 1) / (BM / mg);
+  int ntm = mg == 1 ? (g.M + BM - 1) / BM : (g.M / mg + BM / mg - 1) / (BM / mg);
+  if (EPI == EPI_REFINE && g.mcount && ntm > 8) ntm = 8;   // device-side row count: workgroups loop over M tiles
   if (ntn <= 0 || ntm <= 0 || batch <= 0) return hipSuccess;
   dim3 grid(ntn, ntm, batch);
   hipLaunchKernelGGL((gemm_kernel<CT, TA, TB, TC, TBias, EPI, BM, BN, BK>), grid, dim3(256), 0, st, g);
