@@ -331,9 +331,14 @@ template <> struct Tile<float> { static constexpr int BM = 128, BN = GEMM_BN, BK
 // workgroups fit a CU.
 constexpr int GEMM_LONG_K = 512;
 
-template <class CT, class TA, class TB, class TC, class TBias, int EPI>
+// WIDE: 128 x 256 tiles (BK 32, 2 waves per SIMD) for the latent-side
+// products with many output columns and K >= 512 (fp16 mode; paired kinds need
+// head widths that are multiples of 256).  The norm partials of a PAIR product
+// then number hd/256*2 per head instead of hd/128*2.
+template <class CT, class TA, class TB, class TC, class TBias, int EPI, bool WIDE = false>
 static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st, int cls = STILL_K_LATENT) {
   timing::Scope ts(cls, st);
+  if constexpr (WIDE && sizeof(CT) == 2) return launch_gemm<CT, TA, TB, TC, TBias, EPI, 128, 256, 32>(g, batch, st);
   if (g.K >= GEMM_LONG_K)
     return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
   return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
@@ -426,6 +431,8 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
   const float2* tab_bk = (const float2*)(ws + p.tab_bk);
   const float2* tab_bq = (const float2*)(ws + p.tab_bq);
   const float LOG2E = 1.4426950408889634f;
+  // wide GEMM tiles for the paired projections when the head widths allow them
+  const bool wide_c = !m.fp32 && m.dc % 256 == 0, wide_s = !m.fp32 && m.ns > 0 && m.ds % 256 == 0;
 
   // bf16 mode: the layer's weight matrices converted once to the fp16 MFMA
   // operand type (biases and latents stay bf16); every GEMM then reads fp16.
@@ -520,7 +527,8 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.tab_mod = m.t;
         g.part = partq;
         g.ldpart = Ht;
-        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_QPROJ)));
+        if (wide_c) HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR, true>(g, 1, st, STILL_K_QPROJ)));
+        else HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_QPROJ)));
       }
       {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
         GemmArgs g = gargs((int)HN, m.Ec / 2, m.d2, X, m.d2, bw.ca_wk, m.d2, k, m.Ec);
@@ -536,7 +544,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.ldpart = HN;
         HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_KPROJ)));
       }
-      HIP_TRY(finalize(partq, Ht, m.nc, m.np_c, rq));
+      HIP_TRY(finalize(partq, Ht, m.nc, wide_c ? m.dc / 256 * 2 : m.np_c, rq));
       HIP_TRY(finalize(partk, HN, m.nc, m.np_c, rk));
       const float ca_scale = cfg->logit_scale_cross != 0.f ? cfg->logit_scale_cross : (float)m.dc;
       if constexpr (sizeof(CT) == 2) {   // fold 1/||q~|| * scale * log2(e) into q for the fp16 kernel
@@ -658,7 +666,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
       }
       {  // Z += Concat(heads) W_O^T
         GemmArgs g = gargs((int)Ht, m.D, m.Ec, head, m.Ec, bw.ca_wo, m.Ec, Z, m.D);
-        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID, true>(g, 1, st)));
       }
     }
     // ---------------- latent self-attention: Z += SelfAttn(RMSNorm(Z))
@@ -680,18 +688,20 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.hd = m.ds;
         g.part = partqs;
         g.ldpart = Ht;
-        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
+        if (wide_s) HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR, true>(g, 1, st)));
+        else HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
         g.B = bw.sa_wk;
         g.bias = bw.sa_bk;
         g.C = ks;
         g.part = partks;
-        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
+        if (wide_s) HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR, true>(g, 1, st)));
+        else HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
       }
       {  // v^T[h] = W_V^sa Y[h]^T : [Es][tpad] per KV head
         GemmArgs g = gargs(m.Es, m.t, m.D, bw.sa_wv, m.D, Y, m.D, vT, m.tpad);
         g.sB1 = (long)m.t * m.D;
         g.sC1 = (long)m.Es * m.tpad;
-        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE>(g, m.H, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE, true>(g, m.H, st)));
         if (m.tpad > m.t) {
           TIMED(STILL_K_OTHER);
           hipLaunchKernelGGL((zero_cols_kernel<CT>), dim3(grid1d((long)m.H * m.Es * (m.tpad - m.t))), dim3(256), 0,
@@ -699,8 +709,8 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
           HIP_TRY(hipGetLastError());
         }
       }
-      HIP_TRY(finalize(partqs, Ht, m.ns, m.np_s, rqs));
-      HIP_TRY(finalize(partks, Ht, m.ns, m.np_s, rks));
+      HIP_TRY(finalize(partqs, Ht, m.ns, wide_s ? m.ds / 256 * 2 : m.np_s, rqs));
+      HIP_TRY(finalize(partks, Ht, m.ns, wide_s ? m.ds / 256 * 2 : m.np_s, rks));
       {  // S = s * q k^T with the QK-norm factors, per (h, c)
         GemmArgs g = gargs(m.t, m.t, m.ds, qs, m.Es, ks, m.Es, Ssa, m.tpad);
         g.nb2 = m.ns;
@@ -719,7 +729,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.ldrk = m.ns;
         g.sK1 = (long)m.t * m.ns;
         g.sK2 = 1;
-        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_SCALE>(g, m.H * m.ns, st)));
+        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_SCALE, true>(g, m.H * m.ns, st)));
       }
       {
       TIMED(STILL_K_OTHER);
@@ -749,11 +759,11 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.sB2 = (long)m.ds * m.tpad;
         g.sC1 = (long)m.t * m.Es;
         g.sC2 = m.ds;
-        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE>(g, m.H * m.ns, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE, true>(g, m.H * m.ns, st)));
       }
       {
         GemmArgs g = gargs((int)Ht, m.D, m.Es, Osa, m.Es, bw.sa_wo, m.Es, Z, m.D);
-        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID, true>(g, 1, st)));
       }
     }
     // ---------------- FFN: Z += FFN(RMSNorm(Z))
@@ -763,13 +773,13 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
       if (cfg->ffn_kind == STILL_FFN_SWIGLU) {
         GemmArgs g = gargs((int)Ht, m.F, m.D, Y, m.D, bw.ffn_wg, m.D, hid, m.F);
         g.B2 = bw.ffn_wu;
-        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_SWIGLU>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_SWIGLU, true>(g, 1, st)));
       } else {
         GemmArgs g = gargs((int)Ht, m.F, m.D, Y, m.D, bw.ffn_wu, m.D, hid, m.F);
-        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_GELU>(g, 1, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_GELU, true>(g, 1, st)));
       }
       GemmArgs g = gargs((int)Ht, m.D, m.F, hid, m.F, bw.ffn_wd, m.F, Z, m.D);
-      HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID>(g, 1, st)));
+      HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID, true>(g, 1, st)));
     }
   }
   // ---------------- output heads: C_k = Z_out W_key^T (re-rotated), C_v = Z_out W_val^T
