@@ -121,10 +121,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   // epilogue staging (per wave: 32 rows x TN*32 columns of fp32) must fit the arena
   constexpr int WC = TN * 32;
   constexpr int SLD = WC + 8;                  // staging row stride (floats): rows r and r+4 on disjoint banks
-  static_assert(4 * 32 * SLD * 4 <= gemm_lds_bytes<BM, BN, BK, CT>(), "staging does not fit");
   static_assert(WC == BN / 2, "wave column count");
+  constexpr int LDSB = gemm_lds_bytes<BM, BN, BK, CT>();
+  static_assert(4 * 32 * SLD * 4 <= LDSB, "staging does not fit");
 
-  __shared__ __attribute__((aligned(16))) unsigned char smem[gemm_lds_bytes<BM, BN, BK, CT>()];
+  __shared__ __attribute__((aligned(16))) unsigned char smem[LDSB];
   CT* As = (CT*)smem;                          // [2][BM*LR]
   CT* Bs = As + 2 * BM * LR;                   // [2][BN*LR]
 
@@ -350,20 +351,32 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   for (int a = 0; a < TM; ++a) {
     const int lbase = wm * (BM / 2) + a * 32;    // tile-local first row of the slice
     // ---- 1. values into the staging slice
-    if constexpr (!PAIRED) {
+    if constexpr (EPI == EPI_SCALE) {
+      // per-column and per-row factors loaded once per slice
+      float rkc[TN];
+#pragma unroll
+      for (int b = 0; b < TN; ++b) {
+        const int col = nt * BN + col_base(b) + l32;
+        rkc[b] = col < N ? rkv[(long)col * g.ldrk] * g.scale : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
+        const long r = grow(lbase + rl);
+        const float rqs = r >= 0 ? rqv[r * g.ldrq] : 0.f;
+#pragma unroll
+        for (int b = 0; b < TN; ++b) stg[rl * SLD + b * 32 + l32] = acc[a][b][j] * rqs * rkc[b];
+      }
+    } else if constexpr (!PAIRED) {
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
         const int col = nt * BN + col_base(b) + l32;
         const float bv = (bias && col < N) ? to_f32(bias[col]) : 0.f;
-        const float rk = (EPI == EPI_SCALE && col < N) ? rkv[(long)col * g.ldrk] : 0.f;
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
           float v = acc[a][b][j];
-          if constexpr (EPI == EPI_SCALE) {
-            const long r = grow(lbase + rl);
-            v = (r >= 0 && col < N) ? v * g.scale * rqv[r * g.ldrq] * rk : 0.f;
-          } else if constexpr (EPI == EPI_GELU) {
+          if constexpr (EPI == EPI_GELU) {
             v = gelu_f(v + bv);
           } else if constexpr (EPI != EPI_RESID) {
             v = v + bv;

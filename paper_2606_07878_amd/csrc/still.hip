@@ -662,7 +662,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.sA2 = m.d2;
         g.sB2 = (long)m.dc * m.d2;
         g.sC2 = m.dc;
-        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE>(g, m.nc, st)));
+        HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE, true>(g, m.nc, st)));
       }
       {  // Z += Concat(heads) W_O^T
         GemmArgs g = gargs((int)Ht, m.D, m.Ec, head, m.Ec, bw.ca_wo, m.Ec, Z, m.D);
