@@ -222,3 +222,40 @@ def compact_layer(K: np.ndarray, V: np.ndarray, positions, rope_theta: float, w:
         Ck.append(ck)
         Cv.append(cv)
     return np.stack(Ck), np.stack(Cv), p_q
+
+
+# ----------------------------------------------------------------------------
+# Compositions around one compaction call (Appendix B)
+# ----------------------------------------------------------------------------
+
+def compact_subrange(K: np.ndarray, V: np.ndarray, positions, rope_theta: float, w: dict, cfg, t: int,
+                     start: int, end: int, rerotate: bool = True):
+    """Appendix B recipe with a selected subrange [start, end): only those
+    entries are compacted (to t); the preserved prefix [0, start) and suffix
+    [end, N) are spliced back unchanged around the compact entries, which sit
+    at the evenly spaced output positions of the compacted range.
+
+    Returns (K', V', positions') with N - (end - start) + t entries.
+    """
+    N = K.shape[1]
+    assert 0 <= start < end <= N
+    p = np.asarray(positions, dtype=np.float64)
+    Ck, Cv, pq = compact_layer(K[:, start:end], V[:, start:end], p[start:end], rope_theta, w, cfg, t,
+                               rerotate=rerotate)
+    return (np.concatenate([K[:, :start], Ck, K[:, end:]], axis=1),
+            np.concatenate([V[:, :start], Cv, V[:, end:]], axis=1),
+            np.concatenate([p[:start], pq, p[end:]]))
+
+
+def compact_chunks(K: np.ndarray, V: np.ndarray, positions, rope_theta: float, w: dict, cfg, t: int,
+                   chunk: int, rerotate: bool = True):
+    """Appendix B independent chunk compaction: the range is split into
+    consecutive chunks of `chunk` entries (the last one may be shorter), each
+    compacted to t entries on its own, and the compact chunks concatenated."""
+    N = K.shape[1]
+    assert chunk >= 1
+    p = np.asarray(positions, dtype=np.float64)
+    outs = [compact_layer(K[:, a:a + chunk], V[:, a:a + chunk], p[a:a + chunk], rope_theta, w, cfg, t,
+                          rerotate=rerotate) for a in range(0, N, chunk)]
+    return (np.concatenate([o[0] for o in outs], axis=1), np.concatenate([o[1] for o in outs], axis=1),
+            np.concatenate([o[2] for o in outs]))

@@ -248,3 +248,39 @@ def compact_layer(cfg: configs.CompactorConfig, weights: Dict[str, object], K, V
                                STILL_F_REROTATE if rerotate else 0, Ck, Cv, outp, workspace,
                                workspace.numel(), stream))
     return Ck, Cv, outp
+
+
+def compact_subrange(cfg: configs.CompactorConfig, weights: Dict[str, object], K, V, positions, rope_theta: float,
+                     t: int, start: int, end: int, rerotate: bool = True, mode: int = configs.MODE_BF16):
+    """Compact only the cache entries [start, end) of one layer (to t) and
+    splice the preserved prefix and suffix back around them: returns
+    (K', V', positions') with N - (end - start) + t entries.  The compaction
+    runs through still_compact_layer; slicing and concatenation are copies."""
+    torch = _torch()
+    N = int(K.shape[1])
+    if not (0 <= start < end <= N):
+        raise StillError(-1, f"subrange [{start}, {end}) outside [0, {N})")
+    Ck, Cv, pq = compact_layer(cfg, weights, K[:, start:end].contiguous(), V[:, start:end].contiguous(),
+                               positions[start:end].contiguous(), rope_theta, t, rerotate=rerotate, mode=mode)
+    return (torch.cat([K[:, :start], Ck, K[:, end:]], dim=1), torch.cat([V[:, :start], Cv, V[:, end:]], dim=1),
+            torch.cat([positions[:start], pq, positions[end:]]))
+
+
+def compact_chunks(cfg: configs.CompactorConfig, weights: Dict[str, object], K, V, positions, rope_theta: float,
+                   t: int, chunk: int, rerotate: bool = True, mode: int = configs.MODE_BF16):
+    """Independent chunk compaction: consecutive chunks of `chunk` entries (the
+    last may be shorter) are each compacted to t by still_compact_layer and
+    the compact chunks concatenated in order."""
+    torch = _torch()
+    N = int(K.shape[1])
+    if chunk < 1:
+        raise StillError(-1, "chunk must be >= 1")
+    lw = weights if isinstance(weights, LayerWeights) else LayerWeights(cfg, weights)
+    need = still_workspace_size(make_config(cfg, mode), min(chunk, N), t, 1)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=K.device)   # shared by the chunks (one stream)
+    outs = [compact_layer(cfg, lw, K[:, a:a + chunk].contiguous(), V[:, a:a + chunk].contiguous(),
+                          positions[a:a + chunk].contiguous(), rope_theta, t, rerotate=rerotate, mode=mode,
+                          workspace=ws)
+            for a in range(0, N, chunk)]
+    return (torch.cat([o[0] for o in outs], dim=1), torch.cat([o[1] for o in outs], dim=1),
+            torch.cat([o[2] for o in outs]))

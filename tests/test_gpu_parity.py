@@ -85,7 +85,7 @@ def test_qwen_shapes_reduced_length(wid):
 # evaluates a subset of KV heads (heads are independent in every sublayer).
 # ----------------------------------------------------------------------------
 
-@pytest.mark.parametrize("wid,layer,heads", [(2, 35, [0, 7]), (3, 18, [3]), (4, 0, [5])])
+@pytest.mark.parametrize("wid,layer,heads", [(2, 0, [1, 4]), (2, 18, [2, 6]), (2, 35, [0, 7]), (3, 18, [3]), (4, 0, [5])])
 def test_full_size_layer(wid, layer, heads):
     _case(configs.get_workload(wid), layer=layer, heads=heads, name=f"cfg{wid} full layer {layer} heads {heads}")
 
@@ -124,3 +124,62 @@ def test_config5_first_call_and_teacher_forced_round():
     got1 = run_gpu(w.cfg, rnd, wts, w.rope_theta, w.t)
     ref1 = run_oracle(w.cfg, rnd, wts, w.rope_theta, w.t, heads=heads)
     assert_parity((got1[0][heads], got1[1][heads], got1[2]), ref1, BF16_TOL, what="cfg5 round 1")
+
+
+# ----------------------------------------------------------------------------
+# Appendix B compositions around one compaction call (host-side slicing and
+# concatenation, compaction through still_compact_layer)
+# ----------------------------------------------------------------------------
+
+def _gpu_inputs(cache, wts, mode=configs.MODE_BF16):
+    import torch
+    from tests.helpers import dev_tensor, weights_to_device
+    return (dev_tensor(cache["K"], mode), dev_tensor(cache["V"], mode),
+            torch.from_numpy(cache["positions"]).to("cuda"), weights_to_device(wts, mode))
+
+
+def test_config1_subrange_splice():
+    import torch
+    from oracle import compactor
+    from paper_2606_07878_amd import binding
+    w, t, s, e = W1, 128, 300, 1700
+    log(f"case cfg1 subrange [{s}, {e}) -> t={t}")
+    cache = synth.make_cache(w, 0)
+    wts = synth.make_weights(w, 0, t=t)
+    K, V, pos, W = _gpu_inputs(cache, wts)
+    K2, V2, p2 = binding.compact_subrange(w.cfg, W, K, V, pos, w.rope_theta, t, s, e)
+    torch.cuda.synchronize()
+    c64, w64 = synth.as_f64(cache), synth.as_f64(wts)
+    rK, rV, rp = compactor.compact_subrange(c64["K"], c64["V"], c64["positions"], w.rope_theta, w64, w.cfg, t, s, e)
+    N2 = w.n_tokens - (e - s) + t
+    assert K2.shape[1] == N2 and V2.shape[1] == N2 and p2.shape[0] == N2
+    # preserved prefix / suffix are the input bytes; positions exact
+    assert torch.equal(K2[:, :s], K[:, :s]) and torch.equal(K2[:, s + t:], K[:, e:])
+    assert torch.equal(V2[:, :s], V[:, :s]) and torch.equal(V2[:, s + t:], V[:, e:])
+    p2n = p2.cpu().numpy()
+    np.testing.assert_array_equal(p2n[:s], rp[:s])
+    np.testing.assert_array_equal(p2n[s + t:], rp[s + t:])
+    got = (K2[:, s:s + t].double().cpu().numpy(), V2[:, s:s + t].double().cpu().numpy(), p2[s:s + t].cpu().numpy())
+    assert_parity(got, (rK[:, s:s + t], rV[:, s:s + t], rp[s:s + t]), BF16_TOL, what="cfg1 subrange")
+
+
+@pytest.mark.parametrize("chunk,t", [(512, 64), (700, 48)])
+def test_config1_independent_chunks(chunk, t):
+    import torch
+    from oracle import compactor
+    from paper_2606_07878_amd import binding
+    w = W1
+    log(f"case cfg1 independent chunks of {chunk} -> t={t}")
+    cache = synth.make_cache(w, 0)
+    wts = synth.make_weights(w, 0, t=t)
+    K, V, pos, W = _gpu_inputs(cache, wts)
+    Kc, Vc, pc = binding.compact_chunks(w.cfg, W, K, V, pos, w.rope_theta, t, chunk)
+    torch.cuda.synchronize()
+    c64, w64 = synth.as_f64(cache), synth.as_f64(wts)
+    ref = compactor.compact_chunks(c64["K"], c64["V"], c64["positions"], w.rope_theta, w64, w.cfg, t, chunk)
+    nchunks = -(-w.n_tokens // chunk)
+    assert Kc.shape[1] == nchunks * t
+    for ci in range(nchunks):
+        sl = slice(ci * t, (ci + 1) * t)
+        got = (Kc[:, sl].double().cpu().numpy(), Vc[:, sl].double().cpu().numpy(), pc[sl].cpu().numpy())
+        assert_parity(got, (ref[0][:, sl], ref[1][:, sl], ref[2][sl]), BF16_TOL, what=f"cfg1 chunk {ci}")

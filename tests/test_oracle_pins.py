@@ -384,3 +384,50 @@ def test_kv_bytes_appendix_b():
     for S, gib in [(8192, 1.125), (32768, 4.5), (65536, 9.0), (131072, 18.0)]:
         assert sizing.kv_bytes(36, 8, 128, 2, S) == gib * 2 ** 30
     assert abs(sizing.kv_bytes(36, 8, 128, 2, 328) / 2 ** 20 - 46) < 0.5
+
+
+# --------------------------------------------------------------------------- Appendix B compositions
+
+def test_subrange_and_chunks_reduce_to_one_call():
+    cfg = tiny_cfg()
+    t, N = 3, 9
+    w = rand_weights(cfg, t, std=0.5, rng=np.random.default_rng(21))
+    K, V, pos, th = _layer_inputs(cfg, N, t, rng=np.random.default_rng(22))
+    ref = O.compact_layer(K, V, pos, th, w, cfg, t)
+    for got in (O.compact_subrange(K, V, pos, th, w, cfg, t, 0, N), O.compact_chunks(K, V, pos, th, w, cfg, t, N),
+                O.compact_chunks(K, V, pos, th, w, cfg, t, 5 * N)):
+        for a, b in zip(got, ref):
+            np.testing.assert_array_equal(a, b)
+
+
+def test_subrange_identity_init_is_near_pass_through():
+    """Appendix B splice with the Appendix C identity-style compactor at
+    t = end - start: the spliced cache reproduces the original one."""
+    cfg = configs.get_workload(1).cfg
+    N, s, e = 80, 17, 65
+    t = e - s
+    w = identity_init_weights(cfg, t)
+    rng = np.random.default_rng(23)
+    K = O.rope(rng.normal(size=(cfg.n_kv_heads, N, cfg.head_dim)), np.arange(N, dtype=np.float64), 1e4)
+    V = rng.normal(size=(cfg.n_kv_heads, N, cfg.head_dim))
+    pos = np.arange(N, dtype=np.float64)
+    K2, V2, p2 = O.compact_subrange(K, V, pos, 1e4, w, cfg, t, s, e)
+    np.testing.assert_array_equal(p2, pos)
+    np.testing.assert_array_equal(K2[:, :s], K[:, :s])          # preserved entries untouched
+    np.testing.assert_array_equal(V2[:, e:], V[:, e:])
+    np.testing.assert_allclose(K2, K, rtol=0, atol=2e-5 * np.abs(K).max())
+    np.testing.assert_allclose(V2, V, rtol=0, atol=2e-5 * np.abs(V).max())
+
+
+def test_chunks_identity_init_is_near_pass_through():
+    cfg = configs.get_workload(1).cfg
+    N, chunk = 96, 32
+    w = identity_init_weights(cfg, chunk)
+    rng = np.random.default_rng(24)
+    pos = np.arange(N, dtype=np.float64) * 2.0
+    K = O.rope(rng.normal(size=(cfg.n_kv_heads, N, cfg.head_dim)), pos, 1e6)
+    V = rng.normal(size=(cfg.n_kv_heads, N, cfg.head_dim))
+    K2, V2, p2 = O.compact_chunks(K, V, pos, 1e6, w, cfg, chunk, chunk)
+    np.testing.assert_array_equal(p2, pos)
+    np.testing.assert_allclose(K2, K, rtol=0, atol=2e-5 * np.abs(K).max())
+    np.testing.assert_allclose(V2, V, rtol=0, atol=2e-5 * np.abs(V).max())
