@@ -44,9 +44,9 @@ def measured_traffic(workload_id: int):
     return MEASURED_TRAFFIC["bytes_per_launch"]
 
 
-def ca_flops_per_launch(w) -> float:
+def ca_flops_per_launch(w, N=None) -> float:
     c = w.cfg
-    per_pair = 2.0 * w.t * w.n_tokens * (c.dc + 2 * c.head_dim)
+    per_pair = 2.0 * w.t * (N or w.n_tokens) * (c.dc + 2 * c.head_dim)
     return per_pair * c.n_kv_heads * c.n_cross_heads
 
 
@@ -133,8 +133,6 @@ def main():
     from paper_2606_07878_amd import binding, configs, synth
 
     w = configs.get_workload(args.workload)
-    if w.rounds:
-        raise SystemExit("iterative workloads are benchmarked by their parity tests, not bench.py")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.copy_probe_mib:
@@ -157,11 +155,47 @@ def main():
     outp = torch.empty(t, dtype=torch.float64, device=dev)
     stream = torch.cuda.current_stream(dev)
 
-    def step():
-        st = binding.still_compact_model(ccfg, Ws, Ks, Vs, pos, N, w.rope_theta, t, binding.STILL_F_REROTATE,
+    # Iterative workloads: each round appends fresh tokens to the compact cache
+    # of the previous call and recompacts to t.  The fresh tokens of every
+    # round sit pre-generated behind a t-row slot that takes the previous C_k,
+    # C_v (a device copy); positions likewise.
+    R, Fr = w.rounds, w.fresh_tokens
+    Kr, Vr, Pr = [], [], []
+    for r in range(R):
+        T0 = N + r * Fr
+        fpos = torch.arange(T0, T0 + Fr, dtype=torch.float64, device=dev)
+        kl, vl = [], []
+        for l in range(L):
+            Kf, Vf, _, _ = synth.make_layer_torch(w, 1000 * (r + 1) + l, dev, n_tokens=Fr, positions=fpos,
+                                                   weights=False)
+            kb = torch.empty(w.cfg.n_kv_heads, t + Fr, w.cfg.head_dim, dtype=torch.bfloat16, device=dev)
+            vb = torch.empty_like(kb)
+            kb[:, t:] = Kf
+            vb[:, t:] = Vf
+            kl.append(kb)
+            vl.append(vb)
+        pb = torch.empty(t + Fr, dtype=torch.float64, device=dev)
+        pb[t:] = fpos
+        Kr.append(kl)
+        Vr.append(vl)
+        Pr.append(pb)
+    if R:
+        print(f"[bench] {R} rounds of {Fr} fresh tokens per layer prepared", file=sys.stderr, flush=True)
+
+    def call(Kin, Vin, p, n):
+        st = binding.still_compact_model(ccfg, Ws, Kin, Vin, p, n, w.rope_theta, t, binding.STILL_F_REROTATE,
                                          Ck, Cv, outp, ws, ws_bytes, stream.cuda_stream)
         if st != 0:
             raise binding.StillError(st, binding.still_last_error())
+
+    def step():
+        call(Ks, Vs, pos, N)
+        for r in range(R):
+            for l in range(L):
+                Kr[r][l][:, :t].copy_(Ck[l])
+                Vr[r][l][:, :t].copy_(Cv[l])
+            Pr[r][:t].copy_(outp)
+            call(Kr[r], Vr[r], Pr[r], t + Fr)
 
     for i in range(args.warmup):
         step()
@@ -195,9 +229,11 @@ def main():
             breakdown[name] = round(ms / L, 4)
     binding.still_timing_reset()
 
-    tokens_per_s_layer = N * L / (ms_step / 1e3)
+    tokens_in = N + R * (t + Fr)                        # cache tokens entering the calls of one step
+    tokens_per_s_layer = tokens_in * L / (ms_step / 1e3)
     avg_att_s = att_ms / att_n / 1e3
-    achieved = ca_flops_per_launch(w) / avg_att_s / 1e12
+    launch_flops = (ca_flops_per_launch(w) + R * ca_flops_per_launch(w, t + Fr)) / (1 + R)
+    achieved = launch_flops / avg_att_s / 1e12
     out = {
         "metric": "cache tokens compacted/sec/layer + % HBM BW or % MFMA peak, 1 MI355X",
         "value": round(tokens_per_s_layer, 1),
@@ -206,7 +242,8 @@ def main():
         "ms_per_step": round(ms_step, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f16", "data": "synthetic",
-        "config": {"workload": w.name, "layers": L, "N": N, "t": t, "H_kv": w.cfg.n_kv_heads,
+        "config": {"workload": w.name, "layers": L, "N": N, "t": t, "rounds": R, "fresh_per_round": Fr,
+                   "H_kv": w.cfg.n_kv_heads,
                    "d": w.cfg.head_dim, "D": w.cfg.latent_dim, "n_cross": w.cfg.n_cross_heads,
                    "n_self": w.cfg.n_self_heads, "ffn_hidden": w.cfg.ffn_hidden, "io": "bf16",
                    "parallelism": "single-gpu"},
@@ -215,8 +252,9 @@ def main():
                      "traffic": measured_traffic(args.workload), "traffic_unit": "bytes/launch",
                      "avg_launch_ms": round(avg_att_s * 1e3, 4),
                      "launches": att_n,
-                     "flops_per_launch": ca_flops_per_launch(w)},
-        "layer_mfma_frac": round(layer_flops(w) / (ms_step / L / 1e3) / 1e12 / PEAK_FP16_TFLOPS, 4),
+                     "flops_per_launch": launch_flops},
+        "layer_mfma_frac": round((layer_flops(w) + R * layer_flops(w, t + Fr)) / (ms_step / L / 1e3) / 1e12
+                                 / PEAK_FP16_TFLOPS, 4),
         "kernel_ms_per_layer": breakdown,
     }
     if not args.no_cpu_baseline:

@@ -132,8 +132,9 @@ def _tgen(device, seed: int, layer: int, stream: int):
 
 
 def make_layer_torch(w: Workload, layer: int, device, dtype=None, n_tokens: int | None = None,
-                     positions=None):
-    """(K, V, positions, weights) for one layer as device tensors (bf16 by default)."""
+                     positions=None, weights: bool = True):
+    """(K, V, positions, weights) for one layer as device tensors (bf16 by default);
+    weights is None when not requested (fresh tokens of an iterative round)."""
     import torch
     dtype = dtype or torch.bfloat16
     cfg = w.cfg
@@ -155,8 +156,10 @@ def make_layer_torch(w: Workload, layer: int, device, dtype=None, n_tokens: int 
     a, b = k_free[..., :half], k_free[..., half:]
     K = torch.cat([a * c - b * s, b * c + a * s], dim=-1).to(dtype)
     V = torch.randn(H, N, d, generator=_tgen(device, w.seed, layer, 1), device=device).to(dtype)
+    if not weights:
+        return K, V, positions, None
     g3 = _tgen(device, w.seed, layer, 3)
     from .configs import layer_shapes
-    weights = {k: (torch.randn(*shape, generator=g3, device=device) * WEIGHT_STD).to(dtype)
-               for k, shape in layer_shapes(cfg, w.t).items()}
-    return K, V, positions, weights
+    W = {k: (torch.randn(*shape, generator=g3, device=device) * WEIGHT_STD).to(dtype)
+         for k, shape in layer_shapes(cfg, w.t).items()}
+    return K, V, positions, W
