@@ -63,43 +63,107 @@ __global__ void rope_table_kernel(const double* __restrict__ pos, long R, int w,
 // ---------------------------------------------------------------------------
 // RoPE-fix staging: X[h*N + n] = [R(-p_n) k_n ; v_n] (row-major, 2d wide) and
 // its transpose X^T[h][f][n] (key-contiguous, zero for n in [N, ldxt)).
-// One workgroup per (RW keys, head); the transpose goes through LDS.
+// One workgroup per (RW keys, head).  Rows are read and written in runs of 8
+// elements (16-byte bf16 / fp16 accesses); the transpose goes through LDS and
+// is written in runs of 8 keys.  RW is a multiple of 8 dividing 256.
 // ---------------------------------------------------------------------------
+template <class T> __device__ __forceinline__ void load8(const T* p, float (&o)[8]);
+template <> __device__ __forceinline__ void load8<bf16>(const bf16* p, float (&o)[8]) {
+  const uint4 u = *(const uint4*)p;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    o[2 * i] = __uint_as_float(w[i] << 16);
+    o[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+template <> __device__ __forceinline__ void load8<float>(const float* p, float (&o)[8]) {
+  const f32x4 a = *(const f32x4*)p, b = *(const f32x4*)(p + 4);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    o[i] = a[i];
+    o[4 + i] = b[i];
+  }
+}
+template <class T> __device__ __forceinline__ void store8(T* p, const float (&v)[8]) {
+  T t[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) t[i] = from_f32<T>(v[i]);
+  if constexpr (sizeof(T) == 2) {
+    *(uint4*)p = *(const uint4*)t;
+  } else {
+    *(f32x4*)p = *(const f32x4*)t;
+    *(f32x4*)(p + 4) = *(const f32x4*)(t + 4);
+  }
+}
+
 template <class IT, class CT>
 __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, const IT* __restrict__ V,
                                                       const float2* __restrict__ tab, long N, int d,
                                                       CT* __restrict__ X, CT* __restrict__ XT, long ldxt,
                                                       int RW) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
-  CT* tile = (CT*)smem_raw;              // [RW][2d + 1]
+  CT* tile = (CT*)smem_raw;              // [RW][2d + 8]
   const int h = blockIdx.y;
   const long n0 = (long)blockIdx.x * RW;
-  const int d2 = 2 * d, hh = d / 2, ld = d2 + 1;
+  const int d2 = 2 * d, hh = d / 2, ld = d2 + 8;
   const IT* Kh = K + (long)h * N * d;
   const IT* Vh = V + (long)h * N * d;
-  for (int e = threadIdx.x; e < RW * d2; e += 256) {
-    const int r = e / d2, f = e - r * d2;
+  // phase 1: per row, hh/8 key runs (each giving both rotation halves) and d/8 value runs
+  const int kit = hh / 8, per_row = kit + d / 8;
+  for (int e = threadIdx.x; e < RW * per_row; e += 256) {
+    const int r = e / per_row, q = e - r * per_row;
     const long n = n0 + r;
-    float val = 0.f;
-    if (n < N) {
-      if (f < d) {
-        const int j = f < hh ? f : f - hh;
-        const float2 cs = tab[n * hh + j];
-        const float a = to_f32(Kh[n * d + j]), b = to_f32(Kh[n * d + j + hh]);
-        // inverse rotation: (a, b) -> (a cos + b sin, b cos - a sin)
-        val = f < hh ? a * cs.x + b * cs.y : b * cs.x - a * cs.y;
+    CT* xr = X + ((long)h * N + n) * d2;
+    if (q < kit) {
+      const int j = 8 * q;
+      float y0[8], y1[8];
+      if (n < N) {
+        float a[8], b[8];
+        load8(Kh + n * d + j, a);
+        load8(Kh + n * d + j + hh, b);
+        const f32x4* tp = (const f32x4*)(tab + n * hh + j);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const f32x4 cs = tp[u];   // (cos, sin) of pairs j+2u, j+2u+1
+          // inverse rotation: (a, b) -> (a cos + b sin, b cos - a sin)
+          y0[2 * u] = a[2 * u] * cs[0] + b[2 * u] * cs[1];
+          y1[2 * u] = b[2 * u] * cs[0] - a[2 * u] * cs[1];
+          y0[2 * u + 1] = a[2 * u + 1] * cs[2] + b[2 * u + 1] * cs[3];
+          y1[2 * u + 1] = b[2 * u + 1] * cs[2] - a[2 * u + 1] * cs[3];
+        }
+        store8(xr + j, y0);
+        store8(xr + j + hh, y1);
       } else {
-        val = to_f32(Vh[n * d + (f - d)]);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) y0[u] = y1[u] = 0.f;
       }
-      X[((long)h * N + n) * d2 + f] = from_f32<CT>(val);
+      store8(tile + r * ld + j, y0);
+      store8(tile + r * ld + j + hh, y1);
+    } else {
+      const int f = 8 * (q - kit);
+      float v[8];
+      if (n < N) {
+        load8(Vh + n * d + f, v);
+        store8(xr + d + f, v);
+      } else {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = 0.f;
+      }
+      store8(tile + r * ld + d + f, v);
     }
-    tile[r * ld + f] = from_f32<CT>(val);
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < RW * d2; e += 256) {
-    const int f = e / RW, r = e - f * RW;
-    const long n = n0 + r;
-    if (n < ldxt) XT[((long)h * d2 + f) * ldxt + n] = tile[r * ld + f];
+  // phase 2: X^T rows, 8 keys per store
+  const int runs = RW / 8;
+  for (int e = threadIdx.x; e < d2 * runs; e += 256) {
+    const int f = e / runs, c8 = e - f * runs;
+    const long n = n0 + 8 * c8;
+    if (n >= ldxt) continue;
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = to_f32(tile[(8 * c8 + u) * ld + f]);
+    store8(XT + ((long)h * d2 + f) * ldxt + n, v);
   }
 }
 

@@ -473,8 +473,8 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
   // RoPE-fix staging of X = [R(-p) K ; V] and X^T
   {
     int RW = 64;
-    while (RW > 8 && (size_t)RW * (m.d2 + 1) * m.cs > 32768) RW /= 2;
-    const size_t lds = (size_t)RW * (m.d2 + 1) * m.cs;
+    while (RW > 8 && (size_t)RW * (m.d2 + 8) * m.cs > 40960) RW /= 2;
+    const size_t lds = (size_t)RW * (m.d2 + 8) * m.cs;
     dim3 grid((unsigned)((m.Npad + RW - 1) / RW), m.H);
     TIMED(STILL_K_OTHER);
     hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, tab_bk, m.N,
