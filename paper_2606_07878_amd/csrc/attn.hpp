@@ -276,7 +276,7 @@ namespace still {
 
 // ---------------------------------------------------------------------------
 // fp16 cross-attention, workgroup = TT latents x one key range, NW waves.
-// Key blocks of 256: wave w owns keys [w*256/NW, (w+1)*256/NW) of the block
+// Key blocks of KB (256 or 512): wave w owns keys [w*KB/NW, (w+1)*KB/NW) of the block
 // in the QK product and output features [w*D2/NW, (w+1)*D2/NW) in the P.X
 // product (8 waves keep each wave's accumulators small enough for two waves
 // per SIMD).
@@ -298,10 +298,9 @@ namespace still {
 // are consecutive workgroups of one XCD: they read the same keys through
 // that XCD's L2.
 // ---------------------------------------------------------------------------
-template <int TT, int QC, int D2, int TOPK, int NW>
+template <int TT, int QC, int D2, int TOPK, int NW, int KB = 256>
 __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
   constexpr int LT = TT / 32;            // latent tiles
-  constexpr int KB = 256;                // keys per block
   constexpr int NT = 64 * NW;            // threads
   constexpr int KW = KB / NW;            // keys per wave (QK)
   constexpr int KT = KW / 32;            // key tiles per wave
@@ -576,9 +575,9 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
       l_run[lt] = l_run[lt] * alpha[lt] + lb;
     }
 
-    // ---- O^T += X^T P^T over the block's 256 keys
+    // ---- O^T += X^T P^T over the block's KB keys, 64 at a time
     auto xstep = [&](int s4, half8 (&xc)[FT][4], half8 (&xn)[FT][4]) {
-      if (s4 + 1 < 4) load_x(xn, n0, s4 + 1);
+      if (s4 + 1 < KB / 64) load_x(xn, n0, s4 + 1);
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
 #pragma unroll
@@ -590,10 +589,11 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
         }
       }
     };
-    xstep(0, xA, xB);
-    xstep(1, xB, xA);
-    xstep(2, xA, xB);
-    xstep(3, xB, xA);
+#pragma unroll
+    for (int s4 = 0; s4 < KB / 64; s4 += 2) {
+      xstep(s4, xA, xB);
+      xstep(s4 + 1, xB, xA);
+    }
   }
 
   // ---- partial (O un-normalised, m, l) and the top keys of this key range
