@@ -147,6 +147,74 @@ still_status still_compact_model(const still_config *cfg, int32_t n_layers,
                                  void *const *C_k, void *const *C_v, double *out_positions,
                                  void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Optional bias channel (Appendix A, output projections and beta shaping):
+ * beta[h][i] = Z_out[h][i] . w_beta (Z_out = the final latent state, after the
+ * final RMSNorm when cfg->final_norm), then optionally
+ *   saturation      beta <- beta_max * tanh(beta / beta_max)     (beta_max > 0)
+ *   mass matching   beta <- beta + mass_alpha * log(N / t) + log_x
+ * in that order.  mass_alpha = 1, log_x = 0 is the uniform-attention offset;
+ * log_x = log(x) is the learnable variant (x > 0); mass_alpha scales the
+ * offset (the chunked-compaction sweep of the bias appendix).
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  float beta_max;      /* > 0: saturation; <= 0: off                      */
+  float mass_alpha;    /* factor on log(N / t); 0: no uniform offset      */
+  float log_x;         /* added as is; 0: none                            */
+} still_beta_opts;
+
+/* still_compact_model plus the bias channel.  w_beta: HOST array of n_layers
+ * device pointers to [D] vectors (weight element type); beta: HOST array of
+ * n_layers device [H][t] float32 outputs; beta_opts NULL = no shaping.  All
+ * other arguments, errors and asynchrony as still_compact_model. */
+still_status still_compact_model_beta(const still_config *cfg, int32_t n_layers,
+                                      const still_layer_weights *w,
+                                      const void *const *K, const void *const *V,
+                                      const double *positions, int64_t N, double rope_theta,
+                                      int32_t t, uint32_t flags,
+                                      void *const *C_k, void *const *C_v, double *out_positions,
+                                      const void *const *w_beta, const still_beta_opts *beta_opts,
+                                      float *const *beta,
+                                      void *workspace, size_t workspace_bytes, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Attention of base-model queries over a compacted prefix followed by an
+ * uncompacted suffix, with the optional bias on the compact entries
+ * (Appendix B, bias semantics in attention):
+ *   out = sum_j exp(s_j) v_j / sum_j exp(s_j),
+ *   s_j = scale q . C_k[j] + beta[j] for the t compact entries,
+ *   s_j = scale q . K[j]              for the n_suffix suffix entries.
+ * Queries and keys are taken as given (the caller applies RoPE at logical
+ * positions).  With causal = 1, query i of each query head sits at suffix
+ * position n_suffix - n_queries + i and sees suffix keys up to that position;
+ * all compact entries are visible to every query.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+  int32_t n_kv_heads;   /* H                                                     */
+  int32_t group;        /* query heads per KV head (grouped-query attention), >= 1 */
+  int32_t head_dim;     /* d in {64, 128, 256}                                   */
+  int32_t n_queries;    /* queries per query head; group * n_queries <= 32       */
+  int32_t t;            /* compact entries per KV head, >= 0                     */
+  int32_t n_suffix;     /* suffix entries per KV head, >= 0; t + n_suffix >= 1   */
+  int32_t causal;       /* 0 or 1 (then n_suffix >= n_queries)                   */
+  float scale;          /* logit scale; 0 -> 1/sqrt(d)                           */
+  int32_t mode;         /* still_mode: element type of q, C_k, C_v, K, V, out    */
+} still_attend_config;
+
+/* Bytes of device workspace still_attend needs (0: invalid configuration). */
+size_t still_attend_workspace_size(const still_attend_config *cfg);
+
+/*   q          [H*group][n_queries][d]  (query head h*group + g uses KV head h)
+ *   C_k, C_v   [H][t][d]         (NULL allowed when t = 0)
+ *   beta       [H][t] float32    (NULL = no bias)
+ *   K, V       [H][n_suffix][d]  (NULL allowed when n_suffix = 0)
+ *   out        [H*group][n_queries][d]
+ * All device pointers, 16-byte aligned; errors and asynchrony as the
+ * compaction calls. */
+still_status still_attend(const still_attend_config *cfg, const void *q, const void *C_k, const void *C_v,
+                          const float *beta, const void *K, const void *V, void *out,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
 /* Human-readable name of a status code (static string). */
 const char *still_status_string(int32_t status);
 
@@ -167,8 +235,9 @@ enum {
   STILL_K_QPROJ = 2,        /* cross-attention query projection               */
   STILL_K_REFINE = 3,       /* exact-logit refinement of the top keys         */
   STILL_K_LATENT = 4,       /* latent-side GEMMs (V/O proj, self-attn, FFN, heads) */
-  STILL_K_OTHER = 5,        /* staging, norms, softmax, merge, tables          */
-  STILL_K_COUNT = 6
+  STILL_K_OTHER = 5,        /* staging, norms, softmax, merge, tables, beta    */
+  STILL_K_ATTEND = 6,       /* still_attend: consumer attention and its merge  */
+  STILL_K_COUNT = 7
 };
 still_status still_timing_enable(int32_t class_mask);
 still_status still_timing_reset(void);

@@ -215,6 +215,8 @@ def compact_layer(K: np.ndarray, V: np.ndarray, positions, rope_theta: float, w:
             if trace is not None:
                 trace.setdefault("Z3", []).append(Z.copy())
         Zo = rms_norm(Z, cfg.rms_eps) if cfg.final_norm else Z
+        if trace is not None:
+            trace.setdefault("Zo", []).append(Zo.copy())
         ck = Zo @ w["w_key"].T                    # C_k = Z_out W_key
         cv = Zo @ w["w_val"].T                    # C_v = Z_out W_val
         if rerotate:                              # Appendix B step 5

@@ -54,6 +54,16 @@ class still_layer_weights(ctypes.Structure):
                 ("w_key", ctypes.c_void_p), ("w_val", ctypes.c_void_p)]
 
 
+class still_beta_opts(ctypes.Structure):
+    _fields_ = [("beta_max", ctypes.c_float), ("mass_alpha", ctypes.c_float), ("log_x", ctypes.c_float)]
+
+
+class still_attend_config(ctypes.Structure):
+    _fields_ = [("n_kv_heads", ctypes.c_int32), ("group", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("n_queries", ctypes.c_int32), ("t", ctypes.c_int32), ("n_suffix", ctypes.c_int32),
+                ("causal", ctypes.c_int32), ("scale", ctypes.c_float), ("mode", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -81,6 +91,16 @@ def lib():
                                           ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_void_p),
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
         L.still_compact_model.restype = ctypes.c_int32
+        L.still_compact_model_beta.argtypes = [*L.still_compact_model.argtypes[:13],
+                                               ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(still_beta_opts),
+                                               ctypes.POINTER(ctypes.c_void_p),
+                                               ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.still_compact_model_beta.restype = ctypes.c_int32
+        L.still_attend_workspace_size.argtypes = [ctypes.POINTER(still_attend_config)]
+        L.still_attend_workspace_size.restype = ctypes.c_size_t
+        L.still_attend.argtypes = [ctypes.POINTER(still_attend_config), *[ctypes.c_void_p] * 8, ctypes.c_size_t,
+                                   ctypes.c_void_p]
+        L.still_attend.restype = ctypes.c_int32
         L.still_status_string.argtypes = [ctypes.c_int32]
         L.still_status_string.restype = ctypes.c_char_p
         L.still_last_error.argtypes = []
@@ -156,6 +176,30 @@ def still_compact_model(cfg: still_config, ws: Sequence[LayerWeights], K: Sequen
                                      _ptr(workspace), workspace_bytes, _ptr(stream))
 
 
+def still_compact_model_beta(cfg: still_config, ws: Sequence[LayerWeights], K: Sequence, V: Sequence, positions,
+                             N: int, rope_theta: float, t: int, flags: int, C_k: Sequence, C_v: Sequence,
+                             out_positions, w_beta: Sequence, beta_opts: Optional[still_beta_opts],
+                             beta: Sequence, workspace, workspace_bytes: int, stream) -> int:
+    L = len(ws)
+    wa = (still_layer_weights * L)(*[w.struct for w in ws])
+    arr = lambda xs: (ctypes.c_void_p * L)(*[_ptr(x) for x in xs])  # noqa: E731
+    return lib().still_compact_model_beta(ctypes.byref(cfg), L, wa, arr(K), arr(V), _ptr(positions), N,
+                                          rope_theta, t, flags, arr(C_k), arr(C_v), _ptr(out_positions),
+                                          arr(w_beta), ctypes.byref(beta_opts) if beta_opts is not None else None,
+                                          arr(beta), _ptr(workspace), workspace_bytes, _ptr(stream))
+
+
+def still_attend_workspace_size(cfg: still_attend_config) -> int:
+    return int(lib().still_attend_workspace_size(ctypes.byref(cfg)))
+
+
+def still_attend(cfg: still_attend_config, q, C_k, C_v, beta, K, V, out, workspace, workspace_bytes: int,
+                 stream) -> int:
+    """Raw entry point (pointers or tensors); returns the status code."""
+    return lib().still_attend(ctypes.byref(cfg), _ptr(q), _ptr(C_k), _ptr(C_v), _ptr(beta), _ptr(K), _ptr(V),
+                              _ptr(out), _ptr(workspace), workspace_bytes, _ptr(stream))
+
+
 def still_status_string(status: int) -> str:
     return lib().still_status_string(status).decode()
 
@@ -169,7 +213,7 @@ def still_version() -> str:
 
 
 # kernel classes of the timing facility (still.h)
-KERNEL_CLASSES = {"cross_attn": 0, "kproj": 1, "qproj": 2, "refine": 3, "latent": 4, "other": 5}
+KERNEL_CLASSES = {"cross_attn": 0, "kproj": 1, "qproj": 2, "refine": 3, "latent": 4, "other": 5, "attend": 6}
 
 
 def still_timing_enable(class_mask: int) -> None:
@@ -284,3 +328,55 @@ def compact_chunks(cfg: configs.CompactorConfig, weights: Dict[str, object], K, 
             for a in range(0, N, chunk)]
     return (torch.cat([o[0] for o in outs], dim=1), torch.cat([o[1] for o in outs], dim=1),
             torch.cat([o[2] for o in outs]))
+
+
+def compact_model_beta(cfg: configs.CompactorConfig, weights: List[Dict[str, object]], K: List, V: List,
+                       positions, rope_theta: float, t: int, w_beta: List, beta_max: float = 0.0,
+                       mass_alpha: float = 0.0, log_x: float = 0.0, rerotate: bool = True,
+                       mode: int = configs.MODE_BF16, workspace=None):
+    """compact_model plus the bias head: returns ([C_k], [C_v], out_positions, [beta [H, t] float32])."""
+    torch = _torch()
+    dev = K[0].device
+    ccfg = make_config(cfg, mode)
+    N = int(K[0].shape[1])
+    L = len(K)
+    need = still_workspace_size(ccfg, N, t, L)
+    if need == 0:
+        raise StillError(-5, "configuration rejected by still_workspace_size")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    dt = K[0].dtype
+    Ck = [torch.empty(cfg.n_kv_heads, t, cfg.head_dim, dtype=dt, device=dev) for _ in range(L)]
+    Cv = [torch.empty(cfg.n_kv_heads, t, cfg.head_dim, dtype=dt, device=dev) for _ in range(L)]
+    betas = [torch.empty(cfg.n_kv_heads, t, dtype=torch.float32, device=dev) for _ in range(L)]
+    outp = torch.empty(t, dtype=torch.float64, device=dev)
+    lw = [w if isinstance(w, LayerWeights) else LayerWeights(cfg, w) for w in weights]
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(still_compact_model_beta(ccfg, lw, K, V, positions, N, rope_theta, t,
+                                    STILL_F_REROTATE if rerotate else 0, Ck, Cv, outp, w_beta,
+                                    still_beta_opts(beta_max, mass_alpha, log_x), betas, workspace,
+                                    workspace.numel(), stream))
+    return Ck, Cv, outp, betas
+
+
+def attend(q, C_k, C_v, beta, K, V, group: int = 1, causal: bool = False, scale: float = 0.0, workspace=None):
+    """Attention of q [H*group, n_q, d] over [C_k; K] with bias [beta; 0]
+    through still_attend on the current stream; returns out like q.  C_k/C_v
+    [H, t, d] and K/V [H, S, d] may be None for t = 0 / S = 0; beta [H, t]
+    float32 or None."""
+    torch = _torch()
+    Hq, nq, d = (int(x) for x in q.shape)
+    H = Hq // group
+    t = int(C_k.shape[1]) if C_k is not None else 0
+    S = int(K.shape[1]) if K is not None else 0
+    mode = configs.MODE_FP32 if q.dtype == torch.float32 else configs.MODE_BF16
+    acfg = still_attend_config(H, group, d, nq, t, S, int(causal), float(scale), mode)
+    need = still_attend_workspace_size(acfg)
+    if need == 0:
+        _check(lib().still_attend(ctypes.byref(acfg), *[None] * 8, 0, None))   # raises with the reason
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    out = torch.empty_like(q)
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    _check(still_attend(acfg, q, C_k, C_v, beta, K, V, out, workspace, workspace.numel(), stream))
+    return out

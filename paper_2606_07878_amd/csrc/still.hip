@@ -14,6 +14,7 @@
 #include "../../include/still.h"
 #include "attn.hpp"
 #include "common.hpp"
+#include "consumer.hpp"
 #include "gemm.hpp"
 #include "misc.hpp"
 
@@ -853,8 +854,9 @@ static still_status check_layer(const still_config* c, const Dims& m, const stil
 
 static still_status compact(const still_config* cfg, int32_t L, const still_layer_weights* w, const void* const* K,
                             const void* const* V, const double* positions, int64_t N, double rope_theta, int32_t t,
-                            uint32_t flags, void* const* Ck, void* const* Cv, double* out_positions, void* workspace,
-                            size_t workspace_bytes, void* stream) {
+                            uint32_t flags, void* const* Ck, void* const* Cv, double* out_positions,
+                            const void* const* w_beta, const still_beta_opts* bopt, float* const* beta,
+                            void* workspace, size_t workspace_bytes, void* stream) {
   Dims m;
   still_status s = make_dims(cfg, N, t, &m);
   if (s != STILL_OK) return s;
@@ -871,6 +873,19 @@ static still_status compact(const still_config* cfg, int32_t L, const still_laye
     if (misaligned(K[l]) || misaligned(V[l]) || misaligned(Ck[l]) || misaligned(Cv[l]))
       return fail(STILL_E_INVAL, "layer %d: cache/output pointers must be 16-byte aligned", l);
   }
+  BetaShape shape{0.f, 0.f};
+  if (beta) {
+    if (!w_beta) return fail(STILL_E_INVAL, "beta outputs given without w_beta");
+    for (int l = 0; l < L; ++l)
+      if (!w_beta[l] || !beta[l] || ((uintptr_t)beta[l] & 3u) || ((uintptr_t)w_beta[l] & (m.fp32 ? 3u : 1u)))
+        return fail(STILL_E_INVAL, "layer %d: NULL or misaligned w_beta / beta", l);
+    if (bopt) {
+      if (!std::isfinite(bopt->beta_max) || !std::isfinite(bopt->mass_alpha) || !std::isfinite(bopt->log_x))
+        return fail(STILL_E_INVAL, "beta options must be finite");
+      shape.beta_max = bopt->beta_max > 0.f ? bopt->beta_max : 0.f;
+      shape.offset = (float)(bopt->mass_alpha * std::log((double)N / (double)t) + bopt->log_x);
+    }
+  }
   const Plan p = make_plan(cfg, m);
   if (!workspace) return fail(STILL_E_WORKSPACE, "workspace is NULL");
   if (workspace_bytes < p.total)
@@ -886,8 +901,63 @@ static still_status compact(const still_config* cfg, int32_t L, const still_laye
     s = m.fp32 ? run_layer<float, float>(cfg, m, p, ws, &w[l], K[l], V[l], rerot, Ck[l], Cv[l], st)
                : run_layer<bf16, f16>(cfg, m, p, ws, &w[l], K[l], V[l], rerot, Ck[l], Cv[l], st);
     if (s != STILL_OK) return s;
+    if (beta) {  // beta = shape(Z_out w_beta) from the final latent state left in the workspace
+      TIMED(STILL_K_OTHER);
+      const long rows = (long)m.H * m.t;
+      const float* Z = (const float*)(ws + p.Z);
+      if (m.fp32)
+        hipLaunchKernelGGL((beta_kernel<float>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, Z,
+                           (const float*)w_beta[l], rows, m.D, cfg->final_norm, cfg->rms_eps, shape, beta[l]);
+      else
+        hipLaunchKernelGGL((beta_kernel<bf16>), dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, st, Z,
+                           (const bf16*)w_beta[l], rows, m.D, cfg->final_norm, cfg->rms_eps, shape, beta[l]);
+      if (hipGetLastError() != hipSuccess) return fail(STILL_E_HIP, "beta launch failed");
+    }
   }
   return STILL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Consumer attention over [C_k; K] with bias [beta; 0]
+// ---------------------------------------------------------------------------
+struct AttendPlan {
+  int R, splits;
+  size_t opart, mpart, lpart, total;
+};
+
+static still_status attend_plan(const still_attend_config* c, AttendPlan* ap) {
+  if (!c) return fail(STILL_E_INVAL, "attend config is NULL");
+  if (c->mode != STILL_MODE_BF16 && c->mode != STILL_MODE_FP32) return fail(STILL_E_DTYPE, "unknown mode %d", c->mode);
+  if (c->head_dim != 64 && c->head_dim != 128 && c->head_dim != 256)
+    return fail(STILL_E_UNSUPPORTED, "attend head_dim %d not in {64, 128, 256}", c->head_dim);
+  if (c->n_kv_heads < 1 || c->group < 1 || c->n_queries < 1) return fail(STILL_E_SHAPE, "attend sizes must be >= 1");
+  if ((long)c->group * c->n_queries > ATTEND_MAX_ROWS)
+    return fail(STILL_E_UNSUPPORTED, "group * n_queries = %ld exceeds %d", (long)c->group * c->n_queries,
+                ATTEND_MAX_ROWS);
+  if (c->t < 0 || c->n_suffix < 0 || (long)c->t + c->n_suffix < 1 || (long)c->t + c->n_suffix > (1L << 30))
+    return fail(STILL_E_SHAPE, "attend needs 1 <= t + n_suffix <= 2^30 (t=%d, n_suffix=%d)", c->t, c->n_suffix);
+  if (c->causal != 0 && c->causal != 1) return fail(STILL_E_INVAL, "causal must be 0 or 1");
+  if (c->causal && c->n_suffix < c->n_queries)
+    return fail(STILL_E_SHAPE, "causal attention needs n_suffix >= n_queries");
+  if (!std::isfinite(c->scale) || c->scale < 0.f) return fail(STILL_E_INVAL, "scale must be finite and >= 0");
+  const long total = (long)c->t + c->n_suffix;
+  ap->R = c->group * c->n_queries;
+  ap->splits = (int)((total + 64 * ATTEND_CHUNKS - 1) / (64 * ATTEND_CHUNKS));
+  const size_t slots = (size_t)ap->splits * c->n_kv_heads * ATTEND_MAX_ROWS;
+  ap->opart = 0;
+  ap->mpart = rup((long)(slots * c->head_dim * sizeof(float)), 256);
+  ap->lpart = ap->mpart + rup((long)(slots * sizeof(float)), 256);
+  ap->total = ap->lpart + rup((long)(slots * sizeof(float)), 256) + 256;   // + alignment slack
+  return STILL_OK;
+}
+
+template <class IT, int D>
+static hipError_t launch_attend(const ConsumerArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((attend_partial_kernel<IT, D>), dim3(a.splits, a.H), dim3(64), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((attend_merge_kernel<IT, D>), dim3(a.group * a.nq, a.H), dim3(64), 0, st, a);
+  return hipGetLastError();
 }
 
 }  // namespace still
@@ -910,16 +980,87 @@ still_status still_compact_layer(const still_config* cfg, const still_layer_weig
   const void* Va[1] = {V};
   void* Cka[1] = {C_k};
   void* Cva[1] = {C_v};
-  return compact(cfg, 1, w, Ka, Va, positions, N, rope_theta, t, flags, Cka, Cva, out_positions, workspace,
-                 workspace_bytes, stream);
+  return compact(cfg, 1, w, Ka, Va, positions, N, rope_theta, t, flags, Cka, Cva, out_positions, nullptr, nullptr,
+                 nullptr, workspace, workspace_bytes, stream);
 }
 
 still_status still_compact_model(const still_config* cfg, int32_t n_layers, const still_layer_weights* w,
                                  const void* const* K, const void* const* V, const double* positions, int64_t N,
                                  double rope_theta, int32_t t, uint32_t flags, void* const* C_k, void* const* C_v,
                                  double* out_positions, void* workspace, size_t workspace_bytes, void* stream) {
-  return compact(cfg, n_layers, w, K, V, positions, N, rope_theta, t, flags, C_k, C_v, out_positions, workspace,
-                 workspace_bytes, stream);
+  return compact(cfg, n_layers, w, K, V, positions, N, rope_theta, t, flags, C_k, C_v, out_positions, nullptr,
+                 nullptr, nullptr, workspace, workspace_bytes, stream);
+}
+
+still_status still_compact_model_beta(const still_config* cfg, int32_t n_layers, const still_layer_weights* w,
+                                      const void* const* K, const void* const* V, const double* positions, int64_t N,
+                                      double rope_theta, int32_t t, uint32_t flags, void* const* C_k,
+                                      void* const* C_v, double* out_positions, const void* const* w_beta,
+                                      const still_beta_opts* beta_opts, float* const* beta, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  if (!beta) return fail(STILL_E_INVAL, "beta output array is NULL");
+  return compact(cfg, n_layers, w, K, V, positions, N, rope_theta, t, flags, C_k, C_v, out_positions, w_beta,
+                 beta_opts, beta, workspace, workspace_bytes, stream);
+}
+
+size_t still_attend_workspace_size(const still_attend_config* cfg) {
+  AttendPlan ap;
+  const std::string keep = g_last_error;
+  if (attend_plan(cfg, &ap) != STILL_OK) {
+    g_last_error = keep;
+    return 0;
+  }
+  return ap.total;
+}
+
+still_status still_attend(const still_attend_config* cfg, const void* q, const void* C_k, const void* C_v,
+                          const float* beta, const void* K, const void* V, void* out, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  AttendPlan ap;
+  still_status s = attend_plan(cfg, &ap);
+  if (s != STILL_OK) return s;
+  if ((s = check_ptr(q, "q", true)) != STILL_OK || (s = check_ptr(out, "out", true)) != STILL_OK ||
+      (s = check_ptr(C_k, "C_k", cfg->t > 0)) != STILL_OK || (s = check_ptr(C_v, "C_v", cfg->t > 0)) != STILL_OK ||
+      (s = check_ptr(K, "K", cfg->n_suffix > 0)) != STILL_OK || (s = check_ptr(V, "V", cfg->n_suffix > 0)) != STILL_OK)
+    return s;
+  if (beta && ((uintptr_t)beta & 3u)) return fail(STILL_E_INVAL, "beta is not 4-byte aligned");
+  if (!workspace) return fail(STILL_E_WORKSPACE, "workspace is NULL");
+  if (workspace_bytes < ap.total)
+    return fail(STILL_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, ap.total);
+  char* ws = (char*)(((uintptr_t)workspace + 255) & ~(uintptr_t)255);
+  ConsumerArgs a;
+  a.q = q;
+  a.ck = C_k;
+  a.cv = C_v;
+  a.beta = cfg->t > 0 ? beta : nullptr;
+  a.k = K;
+  a.v = V;
+  a.out = out;
+  a.opart = (float*)(ws + ap.opart);
+  a.mpart = (float*)(ws + ap.mpart);
+  a.lpart = (float*)(ws + ap.lpart);
+  a.H = cfg->n_kv_heads;
+  a.group = cfg->group;
+  a.nq = cfg->n_queries;
+  a.t = cfg->t;
+  a.S = cfg->n_suffix;
+  a.causal = cfg->causal;
+  a.splits = ap.splits;
+  a.scale = cfg->scale != 0.f ? cfg->scale : 1.f / std::sqrt((float)cfg->head_dim);
+  hipStream_t st = (hipStream_t)stream;
+  (void)hipGetLastError();
+  hipError_t e;
+  {
+    TIMED(STILL_K_ATTEND);
+    const bool f32 = cfg->mode == STILL_MODE_FP32;
+    switch (cfg->head_dim) {
+      case 64: e = f32 ? launch_attend<float, 64>(a, st) : launch_attend<bf16, 64>(a, st); break;
+      case 128: e = f32 ? launch_attend<float, 128>(a, st) : launch_attend<bf16, 128>(a, st); break;
+      default: e = f32 ? launch_attend<float, 256>(a, st) : launch_attend<bf16, 256>(a, st); break;
+    }
+  }
+  if (e != hipSuccess) return fail(STILL_E_HIP, "attend launch: %s", hipGetErrorString(e));
+  return STILL_OK;
 }
 
 const char* still_status_string(int32_t s) {

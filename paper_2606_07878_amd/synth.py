@@ -14,8 +14,9 @@ oracle and the GPU path receive identical bits.
 Random streams: numpy PCG64 seeded by SeedSequence([seed, layer, stream]);
 stream 0 = position-free keys, 1 = values, 2 = outlier channel choice,
 3 = weights (fixed enumeration order: latents, block tensors in
-``configs.BLOCK_TENSORS`` order, then w_key, w_val), 10+r = fresh tokens of
-iterative round r.
+``configs.BLOCK_TENSORS`` order, then w_key, w_val), 4 = the bias head's
+w_beta, 5 = consumer-attention operands (queries, compact entries, biases,
+suffix), 10+r = fresh tokens of iterative round r.
 """
 from __future__ import annotations
 
@@ -110,6 +111,28 @@ def make_weights(w: Workload, layer: int, t: int | None = None) -> dict:
                 out[f"b{b}.{name}"] = bf16_bits(r.normal(0.0, WEIGHT_STD, shapes[name]))
     out["w_key"] = bf16_bits(r.normal(0.0, WEIGHT_STD, (cfg.head_dim, cfg.latent_dim)))
     out["w_val"] = bf16_bits(r.normal(0.0, WEIGHT_STD, (cfg.head_dim, cfg.latent_dim)))
+    return out
+
+
+def make_beta_weight(w: Workload, layer: int) -> np.ndarray:
+    """w_beta [latent_dim] of the optional bias head (bf16 bits).  Drawn with
+    std 1/sqrt(latent_dim) so that beta = Z_out w_beta is O(1) on unit-RMS
+    latent states and the bias visibly moves attention."""
+    D = w.cfg.latent_dim
+    return bf16_bits(_rng(w.seed, layer, 4).normal(0.0, 1.0 / np.sqrt(D), D))
+
+
+def make_attend_inputs(seed: int, H: int, group: int, n_q: int, t: int, S: int, d: int,
+                       beta: bool = True) -> dict:
+    """Operands of attention over [C_k; K] with bias [beta; 0] (bf16 bits,
+    beta float32): q [H*group, n_q, d], C_k / C_v [H, t, d], beta [H, t],
+    K / V [H, S, d].  Unit-Gaussian entries (logits q.k/sqrt(d) ~ N(0, 1));
+    beta ~ N(0, 1)."""
+    r = _rng(seed, 0, 5)
+    out = dict(q=bf16_bits(r.standard_normal((H * group, n_q, d))),
+               C_k=bf16_bits(r.standard_normal((H, t, d))), C_v=bf16_bits(r.standard_normal((H, t, d))),
+               K=bf16_bits(r.standard_normal((H, S, d))), V=bf16_bits(r.standard_normal((H, S, d))))
+    out["beta"] = r.standard_normal((H, t)).astype(np.float32) if beta else None
     return out
 
 

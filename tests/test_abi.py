@@ -129,3 +129,72 @@ def test_model_entry_validates_every_layer():
                                           ptrs, ptrs, None, FAKE, 1 << 40, None)
     assert r == -2
     assert "layer 1" in binding.still_last_error()
+
+
+def _beta_call(c, w_beta, beta, opts=None, ws_bytes=1 << 40):
+    w = FakeWeights(c, 256)
+    arr = (binding.still_layer_weights * 1)(w.struct)
+    ptrs = (ctypes.c_void_p * 1)(FAKE)
+    return binding.lib().still_compact_model_beta(
+        ctypes.byref(c), 1, arr, ptrs, ptrs, FAKE, 2048, 1e6, 256, 1, ptrs, ptrs, None,
+        w_beta, ctypes.byref(opts) if opts is not None else None, beta, FAKE, ws_bytes, None)
+
+
+def test_beta_entry_validation():
+    c = _cfg()
+    ok = (ctypes.c_void_p * 1)(FAKE)
+    assert _beta_call(c, ok, None) == -1                               # no beta outputs
+    assert _beta_call(c, None, ok) == -1                               # beta without w_beta
+    assert _beta_call(c, (ctypes.c_void_p * 1)(None), ok) == -1
+    assert _beta_call(c, ok, (ctypes.c_void_p * 1)(FAKE + 2)) == -1    # misaligned float32 output
+    assert _beta_call(c, ok, ok, binding.still_beta_opts(float("nan"), 0.0, 0.0)) == -1
+    assert _beta_call(c, ok, ok, binding.still_beta_opts(2.0, 1.0, -6.9), ws_bytes=16) == -4
+
+
+def _acfg(**kw):
+    base = dict(n_kv_heads=8, group=4, head_dim=128, n_queries=1, t=655, n_suffix=40, causal=0, scale=0.0,
+                mode=configs.MODE_BF16)
+    base.update(kw)
+    return binding.still_attend_config(*[base[f] for f, _ in binding.still_attend_config._fields_])
+
+
+def _attend(c, q=FAKE, ck=FAKE, cv=FAKE, beta=FAKE, k=FAKE, v=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    return binding.lib().still_attend(ctypes.byref(c), q, ck, cv, beta, k, v, out, ws, ws_bytes, None)
+
+
+def test_attend_workspace_size():
+    n = binding.still_attend_workspace_size(_acfg())
+    assert n > 0
+    assert binding.still_attend_workspace_size(_acfg(t=4 * 655)) > n
+    assert binding.still_attend_workspace_size(_acfg(n_queries=9)) == 0    # 36 query rows per KV head
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(mode=5), -3),
+    (dict(head_dim=96), -5),
+    (dict(group=0), -2),
+    (dict(n_queries=9), -5),
+    (dict(t=0, n_suffix=0), -2),
+    (dict(t=-1), -2),
+    (dict(causal=2), -1),
+    (dict(causal=1, n_queries=8, group=2, n_suffix=7), -2),
+    (dict(scale=float("inf")), -1),
+])
+def test_attend_bad_config(kw, status):
+    assert _attend(_acfg(**kw)) == status
+    assert binding.still_last_error()
+
+
+def test_attend_pointer_and_workspace_checks():
+    c = _acfg()
+    assert _attend(c, q=None) == -1
+    assert _attend(c, out=FAKE + 8) == -1
+    assert _attend(c, ck=None) == -1                      # t > 0 needs the compact part
+    assert _attend(c, k=None) == -1                       # n_suffix > 0 needs the suffix
+    assert _attend(c, beta=FAKE + 2) == -1
+    need = binding.still_attend_workspace_size(c)
+    assert _attend(c, ws_bytes=need - 1) == -4
+    assert _attend(c, ws=None) == -4
+    # NULL beta (no bias) and NULL suffix pointers with n_suffix = 0 pass validation
+    c0 = _acfg(n_suffix=0)
+    assert _attend(c0, beta=None, k=None, v=None, ws_bytes=16) == -4

@@ -91,3 +91,63 @@ def test_planted_mistake_is_caught(monkeypatch, name, old, new):
         except Exception as e:  # an assertion, or a shape error the mistake causes
             caught.append(f"{fn.__name__}{kw}: {type(e).__name__}")
     assert caught, f"no pin catches the planted mistake {name}"
+
+
+# ----------------------------------------------------------------------------
+# Bias channel and consumer attention
+# ----------------------------------------------------------------------------
+import oracle.consumer as oracle_consumer  # noqa: E402
+from tests import test_consumer_pins as cpins  # noqa: E402
+
+CONSUMER_SOURCE = inspect.getsource(oracle_consumer)
+
+CONSUMER_MUTATIONS = [
+    ("bias_ignored", "np.zeros(t) if beta is None else np.asarray(beta[h], np.float64)", "np.zeros(t)"),
+    ("bias_on_suffix_too", "np.zeros(S)])", "np.ones(S)])"),
+    ("causal_excludes_diagonal", "logit[t + (S - nq + i) + 1:] = -np.inf", "logit[t + (S - nq + i):] = -np.inf"),
+    ("causal_counts_from_prefix", "logit[t + (S - nq + i) + 1:] = -np.inf", "logit[(S - nq + i) + 1:] = -np.inf"),
+    ("scale_without_sqrt", "(1.0 / math.sqrt(d))", "(1.0 / d)"),
+    ("kv_head_interleaved", "h = hq // group", "h = hq % H"),
+    ("softmax_max_normaliser", "(e @ vals) / e.sum()", "(e @ vals) / e.max()"),
+    ("saturation_unscaled", "b = beta_max * np.tanh(b / beta_max)", "b = np.tanh(b)"),
+    ("mass_ratio_inverted", "math.log(T / t)", "math.log(t / T)"),
+    ("mass_alpha_ignored", "(mass_alpha * math.log(T / t) + log_x)", "(math.log(T / t) + log_x)"),
+]
+
+CONSUMER_PIN_CALLS = [
+    *[(cpins.test_attend_matches_sdpa_with_additive_mask, dict(group=g, causal=c))
+      for g, c in [(1, False), (2, False), (2, True), (3, True)]],
+    (cpins.test_attend_explicit_scale_matches_sdpa, {}),
+    (cpins.test_log_count_bias_equals_duplicated_entries, {}),
+    (cpins.test_uniform_bias_on_empty_suffix_cancels, {}),
+    (cpins.test_single_visible_entry_returns_its_value, {}),
+    (cpins.test_causal_queries_ignore_later_suffix_entries, {}),
+    (cpins.test_beta_head_shaping_closed_forms, {}),
+    *[(cpins.test_beta_head_reads_the_value_heads_state, dict(final_norm=f)) for f in (1, 0)],
+]
+
+
+def _consumer_mutant(old, new):
+    assert CONSUMER_SOURCE.count(old) == 1, f"mutation anchor must occur once: {old!r}"
+    mod = types.ModuleType("oracle_consumer_mutant")
+    mod.__dict__["__package__"] = "oracle"
+    exec(compile(CONSUMER_SOURCE.replace(old, new), "oracle_consumer_mutant", "exec"), mod.__dict__)
+    return mod
+
+
+def test_unmutated_consumer_oracle_passes_every_pin(monkeypatch):
+    monkeypatch.setattr(cpins, "O", oracle_consumer)
+    for fn, kw in CONSUMER_PIN_CALLS:
+        fn(**kw)
+
+
+@pytest.mark.parametrize("name,old,new", CONSUMER_MUTATIONS, ids=[m[0] for m in CONSUMER_MUTATIONS])
+def test_planted_consumer_mistake_is_caught(monkeypatch, name, old, new):
+    monkeypatch.setattr(cpins, "O", _consumer_mutant(old, new))
+    caught = []
+    for fn, kw in CONSUMER_PIN_CALLS:
+        try:
+            fn(**kw)
+        except Exception as e:
+            caught.append(f"{fn.__name__}{kw}: {type(e).__name__}")
+    assert caught, f"no pin catches the planted mistake {name}"
