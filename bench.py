@@ -114,6 +114,67 @@ def copy_probe(mib: int, dev) -> None:
     del src, dst
 
 
+def consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding, reps: int = 20, suffix: int = 64) -> dict:
+    """One decode step of the base model's attention over every layer
+    (query_group query heads per KV head, one query each): over the compact
+    cache [C_k; 64 suffix tokens] with a bias, and over the full uncompacted
+    cache [K; 64 suffix tokens].  The L calls of a step are captured in one
+    HIP graph (as a decode step would run) and the graph is replayed; the time
+    per layer is graph time / L, so launch gaps inside the graph count, host
+    launch costs do not.  Bytes are the algorithmic K and V stream (each entry
+    read once)."""
+    import torch
+    from paper_2606_07878_amd import configs
+    cfg = w.cfg
+    H, d, g, L = cfg.n_kv_heads, cfg.head_dim, w.query_group, len(Ck)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(12345)
+    q = torch.randn(H * g, 1, d, generator=gen, device=dev).to(torch.bfloat16)
+    Ks_sfx = torch.randn(H, suffix, d, generator=gen, device=dev).to(torch.bfloat16)
+    Vs_sfx = torch.randn(H, suffix, d, generator=gen, device=dev).to(torch.bfloat16)
+    beta = torch.randn(H, w.t, generator=gen, device=dev)
+    ws = torch.empty(binding.still_attend_workspace_size(binding.still_attend_config(
+        H, g, d, 1, 0, w.n_tokens + suffix, 0, 0.0, configs.MODE_BF16)), dtype=torch.uint8, device=dev)
+    full_k = [torch.cat([K, Ks_sfx], dim=1) for K in Ks]
+    full_v = [torch.cat([V, Vs_sfx], dim=1) for V in Vs]
+    res = {}
+    for name, args in (("compact", lambda l: (Ck[l], Cv[l], beta, Ks_sfx, Vs_sfx)),
+                       ("full", lambda l: (None, None, None, full_k[l], full_v[l]))):
+        outs = [torch.empty_like(q) for _ in range(L)]
+
+        def step():
+            for l in range(L):
+                binding.attend(q, *args(l), group=g, workspace=ws, out=outs[l])
+        step()                                   # eager warm-up (first-launch costs)
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream(device=dev)
+        s.wait_stream(torch.cuda.current_stream(dev))
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(graph, stream=s):
+                step()
+        torch.cuda.current_stream(dev).wait_stream(s)
+        graph.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            graph.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / (reps * L)
+        entries = (w.t + suffix) if name == "compact" else (w.n_tokens + suffix)
+        nbytes = H * entries * d * 2 * 2
+        res[name] = {"entries": entries, "us_per_layer": round(us, 3), "bytes": nbytes,
+                     "GB_s": round(nbytes / (us * 1e-6) / 1e9, 1),
+                     "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        del graph
+    res["decode_speedup"] = round(res["full"]["us_per_layer"] / res["compact"]["us_per_layer"], 2)
+    res["shape"] = {"H_kv": H, "query_group": g, "n_queries": 1, "d": d, "suffix": suffix, "io": "bf16",
+                    "timing": "HIP graph of the L layer calls, replayed"}
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -123,6 +184,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (HBM counter calibration)")
+    ap.add_argument("--consumer-only", action="store_true",
+                    help="time only the decode attention over the compacted and the full cache (after one "
+                         "compaction step) and print that object")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the compactor forward runs on a "
@@ -201,6 +265,10 @@ def main():
         step()
         torch.cuda.synchronize()
         print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    if args.consumer_only:
+        print(json.dumps({"consumer_attend": consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding),
+                          "config": {"workload": w.name}}), flush=True)
+        return
     binding.still_timing_reset()
     binding.still_timing_enable(1 << binding.KERNEL_CLASSES["cross_attn"])
     e0 = torch.cuda.Event(enable_timing=True)
@@ -218,7 +286,7 @@ def main():
 
     # per-class breakdown (separate, untimed pass)
     binding.still_timing_reset()
-    binding.still_timing_enable((1 << 6) - 1)
+    binding.still_timing_enable((1 << len(binding.KERNEL_CLASSES)) - 1)
     step()
     torch.cuda.synchronize()
     binding.still_timing_enable(0)
@@ -228,6 +296,8 @@ def main():
         if n:
             breakdown[name] = round(ms / L, 4)
     binding.still_timing_reset()
+
+    consumer = consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding)
 
     tokens_in = N + R * (t + Fr)                        # cache tokens entering the calls of one step
     tokens_per_s_layer = tokens_in * L / (ms_step / 1e3)
@@ -256,6 +326,7 @@ def main():
         "layer_mfma_frac": round((layer_flops(w) + R * layer_flops(w, t + Fr)) / (ms_step / L / 1e3) / 1e12
                                  / PEAK_FP16_TFLOPS, 4),
         "kernel_ms_per_layer": breakdown,
+        "consumer_attend": consumer,
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)

@@ -359,11 +359,13 @@ def compact_model_beta(cfg: configs.CompactorConfig, weights: List[Dict[str, obj
     return Ck, Cv, outp, betas
 
 
-def attend(q, C_k, C_v, beta, K, V, group: int = 1, causal: bool = False, scale: float = 0.0, workspace=None):
+def attend(q, C_k, C_v, beta, K, V, group: int = 1, causal: bool = False, scale: float = 0.0, workspace=None,
+           out=None):
     """Attention of q [H*group, n_q, d] over [C_k; K] with bias [beta; 0]
     through still_attend on the current stream; returns out like q.  C_k/C_v
     [H, t, d] and K/V [H, S, d] may be None for t = 0 / S = 0; beta [H, t]
-    float32 or None."""
+    float32 or None.  ``out`` (like q) and ``workspace`` may be given, so that
+    the call allocates nothing (graph capture)."""
     torch = _torch()
     Hq, nq, d = (int(x) for x in q.shape)
     H = Hq // group
@@ -376,7 +378,8 @@ def attend(q, C_k, C_v, beta, K, V, group: int = 1, causal: bool = False, scale:
         _check(lib().still_attend(ctypes.byref(acfg), *[None] * 8, 0, None))   # raises with the reason
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-    out = torch.empty_like(q)
+    if out is None:
+        out = torch.empty_like(q)
     stream = torch.cuda.current_stream(q.device).cuda_stream
     _check(still_attend(acfg, q, C_k, C_v, beta, K, V, out, workspace, workspace.numel(), stream))
     return out

@@ -81,6 +81,7 @@ class Workload:
     outlier_scale: float = 10.0
     rounds: int = 0          # iterative re-compaction rounds after the first call
     fresh_tokens: int = 0    # tokens appended before each round
+    query_group: int = 4     # base-model query heads per KV head (consumer attention)
 
     @property
     def ratio(self) -> float:
@@ -118,7 +119,7 @@ WORKLOADS = {
                             n_cross_heads=8, n_self_heads=8, ffn_kind=FFN_SWIGLU,
                             ffn_hidden=8192),
         n_layers=42, n_tokens=65536, t=1024, rope_theta=1e4, seed=4,
-        rounds=8, fresh_tokens=8192),
+        rounds=8, fresh_tokens=8192, query_group=2),
 }
 
 

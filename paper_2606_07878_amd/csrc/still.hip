@@ -3,6 +3,7 @@
 // sequence of the HIP kernels in gemm.hpp, attn.hpp and misc.hpp.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -921,9 +922,11 @@ static still_status compact(const still_config* cfg, int32_t L, const still_laye
 // Consumer attention over [C_k; K] with bias [beta; 0]
 // ---------------------------------------------------------------------------
 struct AttendPlan {
-  int R, splits;
+  int R, splits, cps, kc;
   size_t opart, mpart, lpart, total;
 };
+
+constexpr int ATTEND_TARGET_BLOCKS = 2048;   // one-wave blocks per launch that keep the chip streaming
 
 static still_status attend_plan(const still_attend_config* c, AttendPlan* ap) {
   if (!c) return fail(STILL_E_INVAL, "attend config is NULL");
@@ -934,16 +937,24 @@ static still_status attend_plan(const still_attend_config* c, AttendPlan* ap) {
   if ((long)c->group * c->n_queries > ATTEND_MAX_ROWS)
     return fail(STILL_E_UNSUPPORTED, "group * n_queries = %ld exceeds %d", (long)c->group * c->n_queries,
                 ATTEND_MAX_ROWS);
+  if (c->n_kv_heads > 65535) return fail(STILL_E_UNSUPPORTED, "n_kv_heads above 65535");
   if (c->t < 0 || c->n_suffix < 0 || (long)c->t + c->n_suffix < 1 || (long)c->t + c->n_suffix > (1L << 30))
     return fail(STILL_E_SHAPE, "attend needs 1 <= t + n_suffix <= 2^30 (t=%d, n_suffix=%d)", c->t, c->n_suffix);
   if (c->causal != 0 && c->causal != 1) return fail(STILL_E_INVAL, "causal must be 0 or 1");
   if (c->causal && c->n_suffix < c->n_queries)
     return fail(STILL_E_SHAPE, "causal attention needs n_suffix >= n_queries");
   if (!std::isfinite(c->scale) || c->scale < 0.f) return fail(STILL_E_INVAL, "scale must be finite and >= 0");
-  const long total = (long)c->t + c->n_suffix;
+  // keys per chunk: the decode kernel's KC (rows <= 8) or the LDS kernel's 64
+  const long R = (long)c->group * c->n_queries;
+  const int esize = c->mode == STILL_MODE_FP32 ? 4 : 2;
+  const int kc = R <= ATTEND_DECODE_ROWS ? (R <= 4 ? 8 : 4) * (64 / (c->head_dim * esize / 16)) : ATTEND_KC;
+  ap->kc = kc;
+  const long chunks = ((long)c->t + kc - 1) / kc + ((long)c->n_suffix + kc - 1) / kc;
+  const long per_head = std::max(1L, (long)ATTEND_TARGET_BLOCKS / c->n_kv_heads);
   ap->R = c->group * c->n_queries;
-  ap->splits = (int)((total + 64 * ATTEND_CHUNKS - 1) / (64 * ATTEND_CHUNKS));
-  const size_t slots = (size_t)ap->splits * c->n_kv_heads * ATTEND_MAX_ROWS;
+  ap->cps = (int)((chunks + per_head - 1) / per_head);
+  ap->splits = (int)((chunks + ap->cps - 1) / ap->cps);
+  const size_t slots = (size_t)ap->splits * c->n_kv_heads * ap->R;
   ap->opart = 0;
   ap->mpart = rup((long)(slots * c->head_dim * sizeof(float)), 256);
   ap->lpart = ap->mpart + rup((long)(slots * sizeof(float)), 256);
@@ -953,10 +964,23 @@ static still_status attend_plan(const still_attend_config* c, AttendPlan* ap) {
 
 template <class IT, int D>
 static hipError_t launch_attend(const ConsumerArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((attend_partial_kernel<IT, D>), dim3(a.splits, a.H), dim3(64), 0, st, a);
+  const int R = a.group * a.nq;
+  const dim3 grid(a.splits, a.H);
+  if (R <= 2)
+    hipLaunchKernelGGL((attend_decode_kernel<IT, D, 2>), grid, dim3(64), 0, st, a);
+  else if (R <= 4)
+    hipLaunchKernelGGL((attend_decode_kernel<IT, D, 4>), grid, dim3(64), 0, st, a);
+  else if (R <= ATTEND_DECODE_ROWS)
+    hipLaunchKernelGGL((attend_decode_kernel<IT, D, 8>), grid, dim3(64), 0, st, a);
+  else if (R <= 16)
+    hipLaunchKernelGGL((attend_partial_kernel<IT, D, 16>), grid, dim3(64), (attend_lds_bytes<IT, D>(16)), st, a);
+  else
+    hipLaunchKernelGGL((attend_partial_kernel<IT, D, ATTEND_MAX_ROWS>), grid, dim3(64),
+                       (attend_lds_bytes<IT, D>(ATTEND_MAX_ROWS)), st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attend_merge_kernel<IT, D>), dim3(a.group * a.nq, a.H), dim3(64), 0, st, a);
+  hipLaunchKernelGGL((attend_merge_kernel<IT, D>), dim3(a.group * a.nq, a.H), dim3(64 * ATTEND_MERGE_WAVES), 0,
+                     st, a);
   return hipGetLastError();
 }
 
@@ -1046,6 +1070,7 @@ still_status still_attend(const still_attend_config* cfg, const void* q, const v
   a.S = cfg->n_suffix;
   a.causal = cfg->causal;
   a.splits = ap.splits;
+  a.cps = ap.cps;
   a.scale = cfg->scale != 0.f ? cfg->scale : 1.f / std::sqrt((float)cfg->head_dim);
   hipStream_t st = (hipStream_t)stream;
   (void)hipGetLastError();

@@ -111,3 +111,52 @@ def test_beta_head_two_layers(mode, final_norm):
         assert np.abs(rb - off).max() > 0.1, "the learned part of the bias should not be negligible"
         assert eb <= tol, f"layer {l}: beta slice error {eb:.3e} > {tol}"
         assert ev <= tol
+
+
+@pytest.mark.parametrize("group,nq,d", [(2, 4, 128), (4, 4, 64), (8, 2, 256), (3, 3, 128)])
+def test_attend_row_bands_causal(group, nq, d):
+    """Query-row counts R = group * n_queries in each register band (<= 4, 8, 16, 32)."""
+    _attend_case(3, group, nq, 777, 129, d, True, configs.MODE_BF16)
+
+
+@pytest.mark.parametrize("group,nq,t,S,d,mode", [
+    (2, 1, 1024, 64, 256, configs.MODE_BF16),     # Gemma-shaped decode: 2 query heads per KV head, d=256
+    (2, 1, 1024, 64, 256, configs.MODE_FP32),
+    (8, 1, 5000, 3, 64, configs.MODE_BF16),       # 8 rows, many chunks and splits
+    (1, 2, 37, 5, 128, configs.MODE_BF16),        # fewer entries than one chunk in each part
+])
+def test_attend_decode_rows(group, nq, t, S, d, mode):
+    _attend_case(4, group, nq, t, S, d, False, mode)
+
+
+def test_attend_graph_replays_match_eager():
+    """The decode calls captured in a HIP graph (as the benchmark times them) give,
+    on every replay, the eager result bit for bit."""
+    import torch
+    from paper_2606_07878_amd import binding
+    a = synth.make_attend_inputs(21, 8, 4, 1, 655, 64, 128)
+    dv = {k: dev_tensor(v, configs.MODE_BF16) for k, v in a.items()}
+    ws = torch.empty(1 << 22, dtype=torch.uint8, device="cuda")
+    qs = [dv["q"] * (1.0 + 0.25 * i) for i in range(3)]
+    eager = [binding.attend(qs[i], dv["C_k"], dv["C_v"], dv["beta"], dv["K"], dv["V"], group=4, workspace=ws)
+             for i in range(3)]
+    outs = [torch.empty_like(q) for q in qs]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for i in range(3):
+                binding.attend(qs[i], dv["C_k"], dv["C_v"], dv["beta"], dv["K"], dv["V"], group=4, workspace=ws,
+                               out=outs[i])
+    torch.cuda.current_stream().wait_stream(s)
+    for rep in range(3):
+        for o in outs:
+            o.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        other = binding.attend(qs[0], dv["C_k"], dv["C_v"], None, dv["K"], dv["V"], group=4, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.isfinite(other.float()).all()
+        for i in range(3):
+            assert torch.equal(outs[i], eager[i]), f"replay {rep}, call {i} differs from eager"
