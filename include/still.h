@@ -184,10 +184,15 @@ still_status still_compact_model_beta(const still_config *cfg, int32_t n_layers,
  *   out = sum_j exp(s_j) v_j / sum_j exp(s_j),
  *   s_j = scale q . C_k[j] + beta[j] for the t compact entries,
  *   s_j = scale q . K[j]              for the n_suffix suffix entries.
- * Queries and keys are taken as given (the caller applies RoPE at logical
- * positions).  With causal = 1, query i of each query head sits at suffix
- * position n_suffix - n_queries + i and sees suffix keys up to that position;
- * all compact entries are visible to every query.
+ * Keys are taken as stored (RoPE'd by the model when they were written).
+ * Queries are taken as given, or, with rope_theta > 0, rotated here by the
+ * base model's RoPE (rotate-half pairs (j, j + d/2), frequency
+ * theta^(-2j/d), angles reduced in fp64) at q_positions: the logical
+ * positions of the queries, i.e. their physical positions plus the offset
+ * T - (physical prefix length) that a compacted cache carries (Appendix B,
+ * logical vs physical cache length).  With causal = 1, query i of each query
+ * head sits at suffix position n_suffix - n_queries + i and sees suffix keys
+ * up to that position; all compact entries are visible to every query.
  * ------------------------------------------------------------------------- */
 typedef struct {
   int32_t n_kv_heads;   /* H                                                     */
@@ -199,19 +204,22 @@ typedef struct {
   int32_t causal;       /* 0 or 1 (then n_suffix >= n_queries)                   */
   float scale;          /* logit scale; 0 -> 1/sqrt(d)                           */
   int32_t mode;         /* still_mode: element type of q, C_k, C_v, K, V, out    */
+  double rope_theta;    /* > 0: rotate q at q_positions; 0: q used as given     */
 } still_attend_config;
 
 /* Bytes of device workspace still_attend needs (0: invalid configuration). */
 size_t still_attend_workspace_size(const still_attend_config *cfg);
 
 /*   q          [H*group][n_queries][d]  (query head h*group + g uses KV head h)
+ *   q_positions [n_queries] fp64 logical positions (required iff rope_theta > 0)
  *   C_k, C_v   [H][t][d]         (NULL allowed when t = 0)
  *   beta       [H][t] float32    (NULL = no bias)
  *   K, V       [H][n_suffix][d]  (NULL allowed when n_suffix = 0)
  *   out        [H*group][n_queries][d]
  * All device pointers, 16-byte aligned; errors and asynchrony as the
  * compaction calls. */
-still_status still_attend(const still_attend_config *cfg, const void *q, const void *C_k, const void *C_v,
+still_status still_attend(const still_attend_config *cfg, const void *q, const double *q_positions,
+                          const void *C_k, const void *C_v,
                           const float *beta, const void *K, const void *V, void *out,
                           void *workspace, size_t workspace_bytes, void *stream);
 

@@ -56,12 +56,19 @@ def compact_layer_beta(K, V, positions, rope_theta: float, w: dict, cfg, t: int,
 
 
 def attend(q: np.ndarray, Ck: np.ndarray, Cv: np.ndarray, beta, K: np.ndarray, V: np.ndarray,
-           group: int = 1, causal: bool = False, scale: float | None = None) -> np.ndarray:
+           group: int = 1, causal: bool = False, scale: float | None = None,
+           q_positions=None, rope_theta: float | None = None) -> np.ndarray:
     """Appendix B: Attn(q; [C_k; K_fix], [C_v; V_fix], [beta; 0]).
 
     q: [H*group, n_q, d]; Ck, Cv: [H, t, d]; beta: [H, t] or None (zeros);
-    K, V: [H, S, d].  Returns [H*group, n_q, d] in float64."""
+    K, V: [H, S, d].  With q_positions ([n_q], logical positions: physical
+    position plus the compacted cache's offset T - physical prefix length,
+    Appendix B "logical vs physical cache length") the queries are first
+    rotated by the base model's RoPE there.  Returns [H*group, n_q, d] in
+    float64."""
     q = np.asarray(q, dtype=np.float64)
+    if q_positions is not None:
+        q = np.stack([compactor.rope(qh, np.asarray(q_positions, np.float64), rope_theta) for qh in q])
     Hq, nq, d = q.shape
     H, t = Ck.shape[0], Ck.shape[1]
     S = K.shape[1]

@@ -61,7 +61,8 @@ class still_beta_opts(ctypes.Structure):
 class still_attend_config(ctypes.Structure):
     _fields_ = [("n_kv_heads", ctypes.c_int32), ("group", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("n_queries", ctypes.c_int32), ("t", ctypes.c_int32), ("n_suffix", ctypes.c_int32),
-                ("causal", ctypes.c_int32), ("scale", ctypes.c_float), ("mode", ctypes.c_int32)]
+                ("causal", ctypes.c_int32), ("scale", ctypes.c_float), ("mode", ctypes.c_int32),
+                ("rope_theta", ctypes.c_double)]
 
 
 _lib = None
@@ -98,7 +99,7 @@ def lib():
         L.still_compact_model_beta.restype = ctypes.c_int32
         L.still_attend_workspace_size.argtypes = [ctypes.POINTER(still_attend_config)]
         L.still_attend_workspace_size.restype = ctypes.c_size_t
-        L.still_attend.argtypes = [ctypes.POINTER(still_attend_config), *[ctypes.c_void_p] * 8, ctypes.c_size_t,
+        L.still_attend.argtypes = [ctypes.POINTER(still_attend_config), *[ctypes.c_void_p] * 9, ctypes.c_size_t,
                                    ctypes.c_void_p]
         L.still_attend.restype = ctypes.c_int32
         L.still_status_string.argtypes = [ctypes.c_int32]
@@ -193,11 +194,11 @@ def still_attend_workspace_size(cfg: still_attend_config) -> int:
     return int(lib().still_attend_workspace_size(ctypes.byref(cfg)))
 
 
-def still_attend(cfg: still_attend_config, q, C_k, C_v, beta, K, V, out, workspace, workspace_bytes: int,
-                 stream) -> int:
+def still_attend(cfg: still_attend_config, q, q_positions, C_k, C_v, beta, K, V, out, workspace,
+                 workspace_bytes: int, stream) -> int:
     """Raw entry point (pointers or tensors); returns the status code."""
-    return lib().still_attend(ctypes.byref(cfg), _ptr(q), _ptr(C_k), _ptr(C_v), _ptr(beta), _ptr(K), _ptr(V),
-                              _ptr(out), _ptr(workspace), workspace_bytes, _ptr(stream))
+    return lib().still_attend(ctypes.byref(cfg), _ptr(q), _ptr(q_positions), _ptr(C_k), _ptr(C_v), _ptr(beta),
+                              _ptr(K), _ptr(V), _ptr(out), _ptr(workspace), workspace_bytes, _ptr(stream))
 
 
 def still_status_string(status: int) -> str:
@@ -360,26 +361,29 @@ def compact_model_beta(cfg: configs.CompactorConfig, weights: List[Dict[str, obj
 
 
 def attend(q, C_k, C_v, beta, K, V, group: int = 1, causal: bool = False, scale: float = 0.0, workspace=None,
-           out=None):
+           out=None, q_positions=None, rope_theta: float = 0.0):
     """Attention of q [H*group, n_q, d] over [C_k; K] with bias [beta; 0]
     through still_attend on the current stream; returns out like q.  C_k/C_v
     [H, t, d] and K/V [H, S, d] may be None for t = 0 / S = 0; beta [H, t]
     float32 or None.  ``out`` (like q) and ``workspace`` may be given, so that
-    the call allocates nothing (graph capture)."""
+    the call allocates nothing (graph capture).  With ``q_positions`` (float64
+    [n_q] device tensor of logical positions) and ``rope_theta`` the kernel
+    rotates q there first."""
     torch = _torch()
     Hq, nq, d = (int(x) for x in q.shape)
     H = Hq // group
     t = int(C_k.shape[1]) if C_k is not None else 0
     S = int(K.shape[1]) if K is not None else 0
     mode = configs.MODE_FP32 if q.dtype == torch.float32 else configs.MODE_BF16
-    acfg = still_attend_config(H, group, d, nq, t, S, int(causal), float(scale), mode)
+    acfg = still_attend_config(H, group, d, nq, t, S, int(causal), float(scale), mode,
+                               float(rope_theta) if q_positions is not None else 0.0)
     need = still_attend_workspace_size(acfg)
     if need == 0:
-        _check(lib().still_attend(ctypes.byref(acfg), *[None] * 8, 0, None))   # raises with the reason
+        _check(lib().still_attend(ctypes.byref(acfg), *[None] * 9, 0, None))   # raises with the reason
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     if out is None:
         out = torch.empty_like(q)
     stream = torch.cuda.current_stream(q.device).cuda_stream
-    _check(still_attend(acfg, q, C_k, C_v, beta, K, V, out, workspace, workspace.numel(), stream))
+    _check(still_attend(acfg, q, q_positions, C_k, C_v, beta, K, V, out, workspace, workspace.numel(), stream))
     return out

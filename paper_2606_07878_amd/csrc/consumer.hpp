@@ -28,9 +28,20 @@ struct ConsumerArgs {
   float* opart;         // [splits][H][R][D]
   float* mpart;         // [splits][H][R]
   float* lpart;
-  int H, group, nq, t, S, causal, splits, cps;   // cps: 64-key chunks per split
+  int H, group, nq, t, S, causal, splits, cps;   // cps: chunks per split
   float scale;
+  const double* qpos;   // [nq] logical query positions, or NULL (q as given)
+  double theta;         // base RoPE theta when qpos is set
 };
+
+// Rotation angle of feature pair jh (< d/2) at position pos, reduced to
+// [-pi, pi] in fp64 before the fp32 sine and cosine (positions reach 1e5+).
+__device__ __forceinline__ void rope_angle(double pos, int jh, int d, double theta, float& c, float& s) {
+  const double inv = pow(theta, -2.0 * jh / d);
+  double phi = pos * inv;
+  phi -= 6.283185307179586 * rint(phi * 0.15915494309189535);
+  sincosf((float)phi, &s, &c);
+}
 
 // Per-(element type, head width) tiling of one chunk.  A key row is PPR
 // 16-byte pieces; the V rows of a chunk are staged through LDS VROWS at a
@@ -139,6 +150,18 @@ __global__ __launch_bounds__(64) void attend_partial_kernel(ConsumerArgs a) {
     }
   }
   __syncthreads();
+  if (a.qpos) {  // RoPE of the query rows at their logical positions (rotate-half pairs)
+    constexpr int HD = D / 2;
+    for (int e = lane; e < R * HD; e += 64) {
+      const int r = e / HD, j = e % HD;
+      float c, sn;
+      rope_angle(a.qpos[r % a.nq], j, D, a.theta, c, sn);
+      const float x0 = qs[r * D + j], x1 = qs[r * D + j + HD];
+      qs[r * D + j] = x0 * c - x1 * sn;
+      qs[r * D + j + HD] = x1 * c + x0 * sn;
+    }
+    __syncthreads();
+  }
 
   float m[RB], l[RB], o[RB][FPL];
 #pragma unroll
@@ -346,6 +369,20 @@ __global__ __launch_bounds__(64) void attend_decode_kernel(ConsumerArgs a) {
       const int rr = min(r, R - 1);
       unpack16<IT>(((const u32x4*)(qh + (long)rr * D))[pl], qv[r]);
       lim[r] = a.causal ? a.S - a.nq + rr % a.nq : 0x7fffffff;   // row g*nq+i sees suffix rows <= S-nq+i
+    }
+    if (a.qpos) {  // RoPE at the logical positions: the pair partner of feature j sits LPK/2 lanes away
+      const bool upper = pl >= TL::LPK / 2;
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        const double pos = a.qpos[min(r, R - 1) % a.nq];
+#pragma unroll
+        for (int e = 0; e < EPP; ++e) {
+          const float other = __shfl_xor(qv[r][e], TL::LPK / 2);
+          float c, sn;
+          rope_angle(pos, (pl % (TL::LPK / 2)) * EPP + e, D, a.theta, c, sn);
+          qv[r][e] = upper ? qv[r][e] * c + other * sn : qv[r][e] * c - other * sn;
+        }
+      }
     }
   }
   float m[RB], l[RB], o[RB][EPP];

@@ -944,6 +944,7 @@ static still_status attend_plan(const still_attend_config* c, AttendPlan* ap) {
   if (c->causal && c->n_suffix < c->n_queries)
     return fail(STILL_E_SHAPE, "causal attention needs n_suffix >= n_queries");
   if (!std::isfinite(c->scale) || c->scale < 0.f) return fail(STILL_E_INVAL, "scale must be finite and >= 0");
+  if (!(c->rope_theta >= 0.0) || !std::isfinite(c->rope_theta)) return fail(STILL_E_INVAL, "rope_theta must be >= 0");
   // keys per chunk: the decode kernel's KC (rows <= 8) or the LDS kernel's 64
   const long R = (long)c->group * c->n_queries;
   const int esize = c->mode == STILL_MODE_FP32 ? 4 : 2;
@@ -1037,9 +1038,9 @@ size_t still_attend_workspace_size(const still_attend_config* cfg) {
   return ap.total;
 }
 
-still_status still_attend(const still_attend_config* cfg, const void* q, const void* C_k, const void* C_v,
-                          const float* beta, const void* K, const void* V, void* out, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+still_status still_attend(const still_attend_config* cfg, const void* q, const double* q_positions,
+                          const void* C_k, const void* C_v, const float* beta, const void* K, const void* V,
+                          void* out, void* workspace, size_t workspace_bytes, void* stream) {
   AttendPlan ap;
   still_status s = attend_plan(cfg, &ap);
   if (s != STILL_OK) return s;
@@ -1048,6 +1049,8 @@ still_status still_attend(const still_attend_config* cfg, const void* q, const v
       (s = check_ptr(K, "K", cfg->n_suffix > 0)) != STILL_OK || (s = check_ptr(V, "V", cfg->n_suffix > 0)) != STILL_OK)
     return s;
   if (beta && ((uintptr_t)beta & 3u)) return fail(STILL_E_INVAL, "beta is not 4-byte aligned");
+  if (cfg->rope_theta > 0.0 && (!q_positions || ((uintptr_t)q_positions & 7u)))
+    return fail(STILL_E_INVAL, "rope_theta > 0 needs 8-byte aligned q_positions");
   if (!workspace) return fail(STILL_E_WORKSPACE, "workspace is NULL");
   if (workspace_bytes < ap.total)
     return fail(STILL_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, ap.total);
@@ -1071,6 +1074,8 @@ still_status still_attend(const still_attend_config* cfg, const void* q, const v
   a.causal = cfg->causal;
   a.splits = ap.splits;
   a.cps = ap.cps;
+  a.qpos = cfg->rope_theta > 0.0 ? q_positions : nullptr;
+  a.theta = cfg->rope_theta;
   a.scale = cfg->scale != 0.f ? cfg->scale : 1.f / std::sqrt((float)cfg->head_dim);
   hipStream_t st = (hipStream_t)stream;
   (void)hipGetLastError();

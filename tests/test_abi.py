@@ -153,13 +153,13 @@ def test_beta_entry_validation():
 
 def _acfg(**kw):
     base = dict(n_kv_heads=8, group=4, head_dim=128, n_queries=1, t=655, n_suffix=40, causal=0, scale=0.0,
-                mode=configs.MODE_BF16)
+                mode=configs.MODE_BF16, rope_theta=0.0)
     base.update(kw)
     return binding.still_attend_config(*[base[f] for f, _ in binding.still_attend_config._fields_])
 
 
-def _attend(c, q=FAKE, ck=FAKE, cv=FAKE, beta=FAKE, k=FAKE, v=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 40):
-    return binding.lib().still_attend(ctypes.byref(c), q, ck, cv, beta, k, v, out, ws, ws_bytes, None)
+def _attend(c, q=FAKE, ck=FAKE, cv=FAKE, beta=FAKE, k=FAKE, v=FAKE, out=FAKE, ws=FAKE, ws_bytes=1 << 40, qpos=None):
+    return binding.lib().still_attend(ctypes.byref(c), q, qpos, ck, cv, beta, k, v, out, ws, ws_bytes, None)
 
 
 def test_attend_workspace_size():
@@ -179,6 +179,7 @@ def test_attend_workspace_size():
     (dict(causal=2), -1),
     (dict(causal=1, n_queries=8, group=2, n_suffix=7), -2),
     (dict(scale=float("inf")), -1),
+    (dict(rope_theta=-1.0), -1),
 ])
 def test_attend_bad_config(kw, status):
     assert _attend(_acfg(**kw)) == status
@@ -195,6 +196,10 @@ def test_attend_pointer_and_workspace_checks():
     need = binding.still_attend_workspace_size(c)
     assert _attend(c, ws_bytes=need - 1) == -4
     assert _attend(c, ws=None) == -4
+    r = _acfg(rope_theta=1e6)
+    assert _attend(r) == -1                                # rotation needs the positions
+    assert _attend(r, qpos=FAKE + 4) == -1                 # fp64 positions, 8-byte aligned
+    assert _attend(r, qpos=FAKE, ws_bytes=16) == -4
     # NULL beta (no bias) and NULL suffix pointers with n_suffix = 0 pass validation
     c0 = _acfg(n_suffix=0)
     assert _attend(c0, beta=None, k=None, v=None, ws_bytes=16) == -4

@@ -124,3 +124,24 @@ def test_beta_head_reads_the_value_heads_state(final_norm):
     ref = compactor.compact_layer(c["K"], c["V"], c["positions"], w.rope_theta, wts, cfg, 6)
     np.testing.assert_allclose(Ck, ref[0], rtol=0, atol=0)
     np.testing.assert_allclose(Cv, ref[1], rtol=0, atol=0)
+
+
+def test_query_rope_at_logical_positions_is_shift_invariant():
+    """Keys stored rotated at their positions, queries rotated at their logical
+    positions: moving every position by the same offset leaves the output
+    unchanged (RoPE's relative-position property), and dropping the query
+    rotation changes it."""
+    f = _inputs(7, H=2, group=2, nq=3, t=5, S=4, d=16)
+    theta = 1e4
+    pc = np.array([0.0, 3.5, 7.0, 10.5, 14.0])          # compact entries at their output positions
+    ps = 20.0 + np.arange(4.0)                             # suffix tokens
+    pq = 24.0 + np.arange(3.0)                             # queries (logical)
+
+    def run(shift, rotate_q=True):
+        Ck = np.stack([compactor.rope(x, pc + shift, theta) for x in f["C_k"]])
+        K = np.stack([compactor.rope(x, ps + shift, theta) for x in f["K"]])
+        return O.attend(f["q"], Ck, f["C_v"], f["beta"], K, f["V"], group=2,
+                        q_positions=(pq + shift) if rotate_q else None, rope_theta=theta)
+    base = run(0.0)
+    np.testing.assert_allclose(run(131072.0 - 14.0), base, rtol=1e-9, atol=1e-11)
+    assert np.abs(run(0.0, rotate_q=False) - base).max() > 1e-2

@@ -23,19 +23,23 @@ pytestmark = pytest.mark.gpu
 ATT_TOL = {configs.MODE_BF16: 8e-3, configs.MODE_FP32: 1e-5}
 
 
-def _attend_case(H, group, nq, t, S, d, causal, mode, beta=True, scale=0.0, seed=11):
+def _attend_case(H, group, nq, t, S, d, causal, mode, beta=True, scale=0.0, seed=11, qpos0=None, theta=1e6):
     import torch
     from oracle import consumer
     from paper_2606_07878_amd import binding
-    name = f"attend H={H} group={group} nq={nq} t={t} S={S} d={d} causal={causal} beta={beta} mode={mode}"
+    name = (f"attend H={H} group={group} nq={nq} t={t} S={S} d={d} causal={causal} beta={beta} mode={mode} "
+            f"qpos0={qpos0}")
     log(name)
     a = synth.make_attend_inputs(seed, H, group, nq, t, S, d, beta=beta)
     f = synth.as_f64(a)
+    qpos = None if qpos0 is None else qpos0 + np.arange(nq, dtype=np.float64)
     ref = consumer.attend(f["q"], f["C_k"], f["C_v"], None if a["beta"] is None else a["beta"].astype(np.float64),
-                          f["K"], f["V"], group=group, causal=causal, scale=scale or None)
+                          f["K"], f["V"], group=group, causal=causal, scale=scale or None,
+                          q_positions=qpos, rope_theta=theta)
     dv = {k: (dev_tensor(v, mode) if v is not None else None) for k, v in a.items()}
     out = binding.attend(dv["q"], dv["C_k"] if t else None, dv["C_v"] if t else None, dv["beta"] if t else None,
-                         dv["K"] if S else None, dv["V"] if S else None, group=group, causal=causal, scale=scale)
+                         dv["K"] if S else None, dv["V"] if S else None, group=group, causal=causal, scale=scale,
+                         q_positions=None if qpos is None else torch.from_numpy(qpos).cuda(), rope_theta=theta)
     torch.cuda.synchronize()
     got = out.double().cpu().numpy()
     assert np.all(np.isfinite(got)), "non-finite output"
@@ -160,3 +164,13 @@ def test_attend_graph_replays_match_eager():
         assert torch.isfinite(other.float()).all()
         for i in range(3):
             assert torch.equal(outs[i], eager[i]), f"replay {rep}, call {i} differs from eager"
+
+
+@pytest.mark.parametrize("group,nq,d,mode", [(4, 1, 128, configs.MODE_BF16), (4, 1, 128, configs.MODE_FP32),
+                                             (2, 3, 256, configs.MODE_BF16), (4, 8, 64, configs.MODE_FP32),
+                                             (3, 5, 128, configs.MODE_BF16)])
+def test_attend_query_rope_at_logical_positions(group, nq, d, mode):
+    """Queries rotated inside the kernel at logical positions past a 128k
+    original prefix (offset T - t carried by the compact cache); both kernels
+    (<= 8 and > 8 query rows)."""
+    _attend_case(2, group, nq, 655, 40, d, True, mode, qpos0=131072.0 + 40 - nq)

@@ -112,6 +112,8 @@ CONSUMER_MUTATIONS = [
     ("saturation_unscaled", "b = beta_max * np.tanh(b / beta_max)", "b = np.tanh(b)"),
     ("mass_ratio_inverted", "math.log(T / t)", "math.log(t / T)"),
     ("mass_alpha_ignored", "(mass_alpha * math.log(T / t) + log_x)", "(math.log(T / t) + log_x)"),
+    ("query_rope_inverted", "compactor.rope(qh, np.asarray(q_positions, np.float64), rope_theta)",
+     "compactor.rope(qh, np.asarray(q_positions, np.float64), rope_theta, inverse=True)"),
 ]
 
 CONSUMER_PIN_CALLS = [
@@ -124,6 +126,7 @@ CONSUMER_PIN_CALLS = [
     (cpins.test_causal_queries_ignore_later_suffix_entries, {}),
     (cpins.test_beta_head_shaping_closed_forms, {}),
     *[(cpins.test_beta_head_reads_the_value_heads_state, dict(final_norm=f)) for f in (1, 0)],
+    (cpins.test_query_rope_at_logical_positions_is_shift_invariant, {}),
 ]
 
 
