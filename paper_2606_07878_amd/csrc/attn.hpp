@@ -24,11 +24,12 @@ struct AttnArgs {
   const void* q;     // [H*t][nc*dc]  rotated, un-normalised queries (CT)
   long ldq;
   const float* rq;   // [H*t][nc]     1 / max(||q~||, eps)
-  const void* k;     // [H*N][nc*dc]  rotated, un-normalised keys (CT)
-  long ldk;
+  const void* k;     // rotated, un-normalised keys (CT): fp32 kernel [H*N][nc*dc] (row stride ldk),
+  long ldk;          //   fp16 kernel the fragment-tiled layout (ktile_off) with npad keys per head
   const float* rk;   // [H*N][nc]
-  const void* xt;    // [H][2d][ldxt] X^T (CT), zero beyond N up to ldxt
+  const void* xt;    // X^T (CT), zero beyond N: fp32 kernel [H][2d][ldxt], fp16 kernel tiled (xtile_off)
   long ldxt;
+  long npad;         // fp16 kernel: keys per head in the tiled layouts (a multiple of 256)
   float* opart;      // [S][H*nc][t][2d]
   float* mpart;      // [S][H*nc][t]
   float* lpart;      // [S][H*nc][t]
@@ -275,59 +276,57 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
 namespace still {
 
 // ---------------------------------------------------------------------------
-// fp16 cross-attention, workgroup = TT latents x one key range, NW waves.
-// Key blocks of KB (256 or 512): wave w owns keys [w*KB/NW, (w+1)*KB/NW) of the block
-// in the QK product and output features [w*D2/NW, (w+1)*D2/NW) in the P.X
-// product (8 waves keep each wave's accumulators small enough for two waves
-// per SIMD).
-//   QK:  S^T[key][lat] over the head width.  Q is staged through LDS in
-//        chunks of QC (one barrier per chunk) and shared by the waves.  K
-//        fragments go from global memory straight into registers (each key
-//        row is read once per workgroup) in groups of 32 of the head width,
-//        through a ring of QC/32 groups: the group used now is reloaded with
-//        the same group of the next chunk, so every K load has a whole chunk
-//        of MFMA work to arrive.  Within a group, lane half g holds the
-//        contiguous run [16g, 16g + 16), so MFMA step s pairs element e of
-//        both operands with width index 16g + 8s + e (any fixed pairing
-//        contracts every index once).
-//   softmax: per-latent block maxima combined across the waves through LDS;
-//        P (fp16) written to LDS as [latent][key].
+// fp16 cross-attention.  Workgroup = TT latents x one key range of one
+// (KV head, cross head) pair; 4 waves, one per SIMD (512 registers each: the
+// logit and output accumulators live in the accumulation registers).  Key
+// blocks of KB = 256; wave w owns keys [64 w, 64 w + 64) of a block in the
+// QK product (64 keys x TT latents per wave) and output features
+// [w D2 / 4, (w + 1) D2 / 4) in the P.X product.
+//   QK: S^T[key][lat] over the head width, in chunks of QC = 64 (one barrier
+//       per chunk).  Q chunks are staged through LDS (three buffers; each
+//       chunk is loaded one chunk ahead of its store), and each step's Q
+//       fragments are read one step ahead of the MFMAs that use them.  K fragments come
+//       from the tiled layout straight into a ring of registers one chunk
+//       deep: the slot used now is reloaded with the same step of the next
+//       chunk (of the next block, in a block's last chunk, so those loads
+//       have the softmax and P.X of the block to arrive).
+//   softmax: logit (log2 units) = S * rk[key]; per-latent block maxima
+//       combined over the 4 waves through LDS; P (fp16) to LDS [lat][key].
 //   P.X: O^T[feat][lat] += X^T[feat][key] P^T[key][lat]; X^T fragments from
-//        global memory (64-byte runs of keys per lane half), P from LDS.
-// 1-D grid ordered so that the t tiles of one (KV head, cross head, split)
-// are consecutive workgroups of one XCD: they read the same keys through
-// that XCD's L2.
+//       the tiled layout through a ring of XR key steps, P from LDS.
+// Keys past the range end (only in its last block) are masked by a select:
+// their tiled k slots may hold stale values.  The grid is 1-D, ordered so
+// that the t tiles of one (pair, split) are consecutive workgroups of one
+// XCD and read the same keys through its L2.
 // ---------------------------------------------------------------------------
-template <int TT, int QC, int D2, int TOPK, int NW, int KB = 256>
-__global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
+template <int TT, int D2, int TOPK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void xattn_f16_kernel(AttnArgs a) {
+  constexpr int NW = 4, NT = 256, KB = 256, KW = 64, KT = 2;
   constexpr int LT = TT / 32;            // latent tiles
-  constexpr int NT = 64 * NW;            // threads
-  constexpr int KW = KB / NW;            // keys per wave (QK)
-  constexpr int KT = KW / 32;            // key tiles per wave
   constexpr int FW = D2 / NW;            // output features per wave
   constexpr int FT = FW / 32;            // feature tiles per wave
-  constexpr int NBK = 2 * NW;            // top-key buckets per latent (wave, lane half)
-  constexpr int G = 32;                  // head-width group of one K load (2 MFMA steps)
-  constexpr int NG = QC / G;             // groups per Q chunk = depth of the K ring
+  constexpr int QC = 64, NS = QC / 16;   // Q chunk width; k steps per chunk = K ring depth
   constexpr int LQ = QC + 8;             // Q stage row stride (halfs)
   constexpr int LP = KB + 8;             // P row stride (halfs)
   constexpr int QV = TT * QC / 8 / NT;   // Q stage vectors per thread
-  static_assert(FT >= 1 && KT >= 1 && QV >= 1 && NG >= 1 && (TT * QC / 8) % NT == 0, "tile sizes");
+  constexpr int NBK = 2 * NW;            // candidate buckets per latent (wave, lane half)
+  constexpr int XR = 4;                  // X^T ring depth (key steps of 16)
+  constexpr int PS = KB / 16;            // key steps per block in P.X
+  static_assert(FT >= 1 && QV >= 1 && (TT * QC / 8) % NT == 0, "tile sizes");
 
-  __shared__ __attribute__((aligned(16))) f16 Qs[2][TT * LQ];
+  __shared__ __attribute__((aligned(16))) f16 Qs[3][TT * LQ];
   __shared__ __attribute__((aligned(16))) f16 Ps[TT * LP];
   __shared__ float red_m[TT][NW], red_l[TT][NW];
-  __shared__ float2 rks[KB];   // (1/||k~||, 0) or (0, -inf) past the key range
+  __shared__ __attribute__((aligned(16))) float rks[2][KB];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   const int l32 = lane & 31, lg = lane >> 5;
 
   const int ntt = (a.t + TT - 1) / TT, HC = a.H * a.nc;
   const int total = gridDim.x;
   int L = blockIdx.x;
   if ((total & 7) == 0) L = (L & 7) * (total >> 3) + (L >> 3);
-  // order: latent tile fastest, then split, then (KV head, cross head): the
-  // workgroups an XCD runs at once share one Q tile set and few key ranges
   const int S = total / (ntt * HC);
   const int tt = L % ntt, rest = L / ntt;
   const int split = rest % S, hc = rest / S;
@@ -337,12 +336,12 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
   const int nend = min(a.N, nbeg + a.keys_per_split);
 
   const f16* qb = (const f16*)a.q + (long)h * a.t * a.ldq + (long)c * a.dc;
-  const f16* kb = (const f16*)a.k + (long)h * a.N * a.ldk + (long)c * a.dc;
-  const f16* xtb = (const f16*)a.xt + (long)h * a.d2 * a.ldxt;
+  const f16* kb = (const f16*)a.k + (long)hc * a.npad * a.dc;
+  const f16* xtb = (const f16*)a.xt + (long)h * a.d2 * a.npad;
   const float* rkb = a.rk + (long)h * a.N * a.nc + c;
+  const unsigned ksteps = (unsigned)(a.dc >> 4);   // width steps of one key tile
+  const unsigned nsteps = (unsigned)(a.npad >> 4); // key steps of one feature tile
 
-  // q arrives pre-scaled by 1/||q~|| * scale * log2(e) (qprescale_kernel), so a
-  // logit in log2 units is S^T * rk[key]
   float m_run[LT], l_run[LT];
 #pragma unroll
   for (int lt = 0; lt < LT; ++lt) {
@@ -375,10 +374,7 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
     }
   }
 
-  // Loads address uniform bases (q, k, X^T of this head) with 32-bit element
-  // offsets (the host bounds them), and are branch-free: rows past the end
-  // read the last valid row, whose values are then zeroed (Q) or masked out
-  // of the softmax (K), so the number of loads in flight stays static.
+  // Q chunk staging (rows past t read the last row and are stored as zeros)
   half8 qreg[QV];
   auto load_q = [&](int d0) {
 #pragma unroll
@@ -395,77 +391,115 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
       *(half8*)&Qs[buf][r * LQ + kk] = (t0 + r < a.t) ? qreg[i] : zero_frag<f16>();
     }
   };
-  // K fragments of this wave's keys for one group of 32: [key tile][step]
-  unsigned krow[KT];
-#pragma unroll
-  for (int kt = 0; kt < KT; ++kt) krow[kt] = 0;
-  auto set_krows = [&](int n0) {
-#pragma unroll
-    for (int kt = 0; kt < KT; ++kt) {
-      const unsigned n = (unsigned)min(n0 + KW * w + 32 * kt + l32, nend - 1);
-      krow[kt] = n * (unsigned)a.ldk + 16u * lg;
-    }
+  // K fragment of this wave's key tile kt of the block at n0, width step js
+  auto load_k = [&](int n0, int kt, int js) -> half8 {
+    const unsigned kti = (unsigned)(n0 + KW * w + 32 * kt) >> 5;
+    return *(const half8*)(kb + ((kti * ksteps + (unsigned)js) * 512u + 8u * lane));
   };
-  auto load_kg = [&](half8 (&kr)[KT][2], int d0) {
-#pragma unroll
-    for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-      for (int s = 0; s < 2; ++s) kr[kt][s] = *(const half8*)(kb + (krow[kt] + (unsigned)(d0 + 8 * s)));
+  // X^T fragment of this wave's feature tile f, key step ns (absolute)
+  auto load_x = [&](int f, int ns) -> half8 {
+    const unsigned ft = (unsigned)(FW / 32 * w + f);
+    return *(const half8*)(xtb + ((ft * nsteps + (unsigned)ns) * 512u + 8u * lane));
   };
-  // X^T fragments for P.X step group s4: [feature tile][step]
-  auto load_x = [&](half8 (&xr)[FT][4], int n0, int s4) {
-#pragma unroll
-    for (int f = 0; f < FT; ++f) {
-      const unsigned fr = FW * w + 32 * f + l32;
-      const unsigned off = fr * (unsigned)a.ldxt + (unsigned)(n0 + 64 * s4 + 32 * lg);
-#pragma unroll
-      for (int s = 0; s < 4; ++s) xr[f][s] = *(const half8*)(xtb + (off + 8u * s));   // X^T padded to the block size
-    }
+  auto load_rk = [&](int n0) -> float {   // 0 past the range end (branch-free load)
+    const int n = n0 + tid;
+    const float v = rkb[(long)min(n, nend - 1) * a.nc];
+    return n < nend ? v : 0.f;
   };
 
-  const int nch = a.dc / QC;   // a.dc is a multiple of QC (checked on the host)
-  half8 kr[NG][KT][2];
-  half8 xA[FT][4], xB[FT][4];
+  const int nch = a.dc / QC;   // a.dc is a multiple of QC (checked on the host), nch >= 2
+  half8 kr[NS][KT];
+  half8 xr[XR][FT];
+  half8 qf[2][LT];
+  // Q chunks rotate through 3 LDS buffers: the chunk in use (qb0), the next
+  // one (qb1, already visible, so the first fragments of the next chunk can be
+  // read before the chunk boundary) and the one being staged (qb2, Q chunk
+  // qn2 of the head width, loaded one chunk ahead of its store).
+  int qb0 = 0, qb1 = 1, qb2 = 2, qn2 = 2 % nch;
+  int rbuf = 0;
+  // prologue: Q chunks 0 and 1, key norms and K ring of the first block
+  load_q(0);
+  store_q(0);
+  load_q(QC);
+  store_q(1);
+#pragma unroll
+  for (int j = 0; j < NS; ++j)
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) kr[j][kt] = load_k(nbeg, kt, j);
+  rks[0][tid] = load_rk(nbeg);
+  __syncthreads();
+#pragma unroll
+  for (int lt = 0; lt < LT; ++lt) qf[0][lt] = *(const half8*)&Qs[0][(32 * lt + l32) * LQ + 8 * lg];
+
   for (int n0 = nbeg; n0 < nend; n0 += KB) {
+    const bool next_block = n0 + KB < nend;   // uniform
     f32x16 s[LT][KT];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt)
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) s[lt][kt] = zero16();
-    load_q(0);
-    set_krows(n0);
+
+    // ---- S^T = K_blk Q^T over the head width.  A chunk runs its MFMAs on the
+    // Q chunk in LDS and the K ring while it loads the next stages: Q chunk
+    // qn2 (stored at the chunk's end) and, into each ring slot right after its
+    // last use, the same step of the next chunk (k steps ks0 + j of the block
+    // at kn0).  Each step reads the next step's Q fragments (the next chunk's
+    // first ones in the last step) before its own MFMAs; scheduling barriers
+    // keep that order and spread the loads over the chunk.
+    auto qk_chunk = [&](int kn0, int ks0) {
+      load_q(qn2 * QC);
+      const f16* Qc = Qs[qb0];
+      const f16* Qn = Qs[qb1];
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) load_kg(kr[gi], gi * G);
-    store_q(0);
-    for (int i = tid; i < KB; i += NT) {
-      const int n = n0 + i;
-      rks[i] = n < nend ? make_float2(rkb[(long)n * a.nc], 0.f) : make_float2(0.f, -INFINITY);
-    }
-    __syncthreads();
-    for (int c = 0; c < nch; ++c) {
-      const int cur = c & 1;
-      const bool more = c + 1 < nch;
-      if (more) load_q((c + 1) * QC);
-      else load_x(xA, n0, 0);
+      for (int j = 0; j < NS; ++j) {
+        const f16* src = (j + 1 < NS) ? Qc : Qn;
+        const int col = (j + 1 < NS) ? 16 * (j + 1) : 0;
 #pragma unroll
-      for (int gi = 0; gi < NG; ++gi) {
+        for (int lt = 0; lt < LT; ++lt)
+          qf[(j + 1) & 1][lt] = *(const half8*)&src[(32 * lt + l32) * LQ + col + 8 * lg];
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int st = 0; st < 2; ++st) {
+        for (int lt = 0; lt < LT; ++lt)
 #pragma unroll
-          for (int lt = 0; lt < LT; ++lt) {
-            const half8 bq = *(const half8*)&Qs[cur][(32 * lt + l32) * LQ + gi * G + 16 * lg + 8 * st];
+          for (int kt = 0; kt < KT; ++kt)
+            s[lt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[j][kt], qf[j & 1][lt], s[lt][kt], 0, 0, 0);
 #pragma unroll
-            for (int kt = 0; kt < KT; ++kt)
-              s[lt][kt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[gi][kt][st], bq, s[lt][kt], 0, 0, 0);
-          }
-        }
-        if (more) load_kg(kr[gi], (c + 1) * QC + gi * G);
+        for (int kt = 0; kt < KT; ++kt) kr[j][kt] = load_k(kn0, kt, ks0 + j);
+        __builtin_amdgcn_sched_barrier(0);
       }
-      if (more) store_q(cur ^ 1);
+      store_q(qb2);
+      const int t = qb0;
+      qb0 = qb1;
+      qb1 = qb2;
+      qb2 = t;
+      qn2 = qn2 + 1 == nch ? 0 : qn2 + 1;
+    };
+    for (int ch = 0; ch + 1 < nch; ++ch) {
+      qk_chunk(n0, (ch + 1) * NS);
       __syncthreads();
     }
+    {  // last chunk: the next stage is chunk 0 of the next block (of this block
+       // again at the very end: loaded, never used), with its key norms
+      const float rk_next = load_rk(n0 + KB);
+      qk_chunk(next_block ? n0 + KB : n0, 0);
+      rks[rbuf ^ 1][tid] = rk_next;
+      __syncthreads();
+    }
+    // X^T ring for the block's P.X (arrives during the softmax)
+#pragma unroll
+    for (int i = 0; i < XR; ++i)
+#pragma unroll
+      for (int f = 0; f < FT; ++f) xr[i][f] = load_x(f, (n0 >> 4) + i);
 
-    // ---- softmax statistics for the block: logit (log2 units) = S * rk + mask
+    // ---- softmax: logit (log2 units) = S * rk, masked past the range end.  The
+    // logits stay in the accumulators: one pass for the block maxima, one for
+    // the probabilities (the refinement candidates recompute them, rarely).
+    const float* rkc = rks[rbuf];
+    const bool tail = n0 + KB > nend;
+    auto logit = [&](int lt, int kt, int j, float rk) -> float {
+      const float x = s[lt][kt][j] * rk;
+      return (tail && n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3) >= nend) ? -INFINITY : x;
+    };
     float mx[LT], lmx[LT];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) mx[lt] = -INFINITY;
@@ -473,17 +507,12 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
     for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
-        // keys KW*w + 32*kt + 8*jq + 4*lg + (0..3): two 16-byte LDS reads
-        const float4 r01 = *(const float4*)&rks[KW * w + 32 * kt + 8 * jq + 4 * lg];
-        const float4 r23 = *(const float4*)&rks[KW * w + 32 * kt + 8 * jq + 4 * lg + 2];
-        const float rk[4] = {r01.x, r01.z, r23.x, r23.z}, mk[4] = {r01.y, r01.w, r23.y, r23.w};
+        const float4 r4 = *(const float4*)&rkc[KW * w + 32 * kt + 8 * jq + 4 * lg];   // keys of j = 4 jq + u
+        const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
 #pragma unroll
-        for (int lt = 0; lt < LT; ++lt) {
+        for (int lt = 0; lt < LT; ++lt)
 #pragma unroll
-          for (int u = 0; u < 4; ++u) s[lt][kt][4 * jq + u] = fmaf(s[lt][kt][4 * jq + u], rk[u], mk[u]);
-          mx[lt] = fmaxf(fmaxf(mx[lt], fmaxf(s[lt][kt][4 * jq], s[lt][kt][4 * jq + 1])),
-                         fmaxf(s[lt][kt][4 * jq + 2], s[lt][kt][4 * jq + 3]));
-        }
+          for (int u = 0; u < 4; ++u) mx[lt] = fmaxf(mx[lt], logit(lt, kt, 4 * jq + u, rk[u]));
       }
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
@@ -507,10 +536,12 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
       for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
         for (int jq = 0; jq < 4; ++jq) {
+          const float4 r4 = *(const float4*)&rkc[KW * w + 32 * kt + 8 * jq + 4 * lg];
+          const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
           half4 pv;
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float p = __builtin_amdgcn_exp2f(s[lt][kt][4 * jq + u] - mref);
+            const float p = __builtin_amdgcn_exp2f(logit(lt, kt, 4 * jq + u, rk[u]) - mref);
             ps += p;
             pv[u] = (f16)p;
           }
@@ -531,9 +562,11 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
             tv[q] = cv[q];
             ti[q] = ci[q];
           }
+#pragma unroll
           for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
             for (int j = 0; j < 16; ++j) {
-              float v = s[lt][kt][j];
+              float v = logit(lt, kt, j, rkc[KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3)]);
               if (v > fmaxf(tv[TOPK - 1], cut0)) {
                 int id = n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
 #pragma unroll
@@ -557,13 +590,6 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
         }
       }
       m_run[lt] = m_new;
-      // rescale only when some latent of the tile saw a new maximum
-      if (__any(alpha[lt] != 1.f)) {
-#pragma unroll
-        for (int f = 0; f < FT; ++f)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) o[f][lt][j] *= alpha[lt];
-      }
     }
     __syncthreads();
 #pragma unroll
@@ -574,29 +600,49 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
       for (int u = 0; u < NW; ++u) lb += red_l[li][u];
       l_run[lt] = l_run[lt] * alpha[lt] + lb;
     }
-
-    // ---- O^T += X^T P^T over the block's KB keys, 64 at a time
-    auto xstep = [&](int s4, half8 (&xc)[FT][4], half8 (&xn)[FT][4]) {
-      if (s4 + 1 < KB / 64) load_x(xn, n0, s4 + 1);
+    rbuf ^= 1;
+    // rescale O for the latents whose maximum grew (rare after the first
+    // blocks), one 32x32 tile at a time
 #pragma unroll
-      for (int st = 0; st < 4; ++st) {
+    for (int lt = 0; lt < LT; ++lt) {
+      if (__any(alpha[lt] != 1.f)) {
 #pragma unroll
-        for (int lt = 0; lt < LT; ++lt) {
-          const half8 bp = *(const half8*)&Ps[(32 * lt + l32) * LP + 64 * s4 + 32 * lg + 8 * st];
+        for (int f = 0; f < FT; ++f) {
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int f = 0; f < FT; ++f)
-            o[f][lt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(xc[f][st], bp, o[f][lt], 0, 0, 0);
+          for (int j = 0; j < 16; ++j) o[f][lt][j] *= alpha[lt];
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
-    };
+    }
+
+    // ---- O^T += X^T P^T over the block's KB keys, 16 at a time (the next
+    // step's P fragments read before this step's MFMAs)
+    half8 pf[2][LT];
 #pragma unroll
-    for (int s4 = 0; s4 < KB / 64; s4 += 2) {
-      xstep(s4, xA, xB);
-      xstep(s4 + 1, xB, xA);
+    for (int lt = 0; lt < LT; ++lt) pf[0][lt] = *(const half8*)&Ps[(32 * lt + l32) * LP + 8 * lg];
+#pragma unroll
+    for (int ps = 0; ps < PS; ++ps) {
+      if (ps + 1 < PS) {
+#pragma unroll
+        for (int lt = 0; lt < LT; ++lt)
+          pf[(ps + 1) & 1][lt] = *(const half8*)&Ps[(32 * lt + l32) * LP + 16 * (ps + 1) + 8 * lg];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int lt = 0; lt < LT; ++lt)
+#pragma unroll
+        for (int f = 0; f < FT; ++f)
+          o[f][lt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(xr[ps % XR][f], pf[ps & 1][lt], o[f][lt], 0, 0, 0);
+      if (ps + XR < PS) {
+#pragma unroll
+        for (int f = 0; f < FT; ++f) xr[ps % XR][f] = load_x(f, (n0 >> 4) + ps + XR);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
-  // ---- partial (O un-normalised, m, l) and the top keys of this key range
+  // ---- partial (O un-normalised, m, l) of this key range
 #pragma unroll
   for (int lt = 0; lt < LT; ++lt) {
     const int lat = t0 + 32 * lt + l32;
@@ -615,4 +661,3 @@ __global__ __launch_bounds__(64 * NW) void xattn_f16_kernel(AttnArgs a) {
 }
 
 }  // namespace still
-

@@ -106,6 +106,27 @@ template <> struct VecLoad<float, float> {
   static __device__ __forceinline__ f32x4 load(const float* p) { return *(const f32x4*)p; }
 };
 
+// ---------------------------------------------------------------------------
+// Fragment-tiled layouts of the fp16 cross-attention operands.  One MFMA
+// operand fragment (64 lanes x 8 halfs: 32 rows x 16 contraction indices) is
+// 1 KB of contiguous memory, so each fragment load of a wave is one fully
+// coalesced 1 KB read.  Lane l of a fragment holds row l % 32 and contraction
+// indices 8 * (l / 32) + [0, 8) of the fragment's 16.
+//   k (projected keys) of KV head h, cross head c (hc = h * nc + c), key n,
+//   width index x (npad keys per head, a multiple of 256):
+//     [hc][n / 32][x / 16][lane = n % 32 + 32 * ((x / 8) % 2)][x % 8]
+//   X^T of KV head h, feature f, key n:
+//     [h][f / 32][n / 16][lane = f % 32 + 32 * ((n / 8) % 2)][n % 8]
+// ---------------------------------------------------------------------------
+__host__ __device__ __forceinline__ long ktile_off(long hc, long n, long x, long npad, long dc) {
+  return ((((hc * (npad >> 5) + (n >> 5)) * (dc >> 4) + (x >> 4)) << 9) + (((n & 31) + (((x >> 3) & 1) << 5)) << 3) +
+          (x & 7));
+}
+__host__ __device__ __forceinline__ long xtile_off(long h, long f, long n, long npad, long d2) {
+  return ((((h * (d2 >> 5) + (f >> 5)) * (npad >> 4) + (n >> 4)) << 9) + (((f & 31) + (((n >> 3) & 1) << 5)) << 3) +
+          (n & 7));
+}
+
 // Keys whose fp16-path logit lies within this many log2 units of their row's
 // maximum are candidates for the exact-logit refinement of cross-attention.
 constexpr float REFINE_MARGIN = 10.f;

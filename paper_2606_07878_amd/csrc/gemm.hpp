@@ -57,6 +57,11 @@ struct GemmArgs {
   float* part;         // PAIR: sum-of-squares partials [head*nparts + p][ldpart] (ldpart >= rows), NULL = none
   long ldpart;
   float* C2;           // PAIR: optional fp32 copy of the (rotated) outputs, ldc as C
+  // PAIR: with kt_n > 0, C is written in the fragment-tiled key layout of the
+  // fp16 cross-attention (ktile_off): row r = h * kt_n + n (KV head h, key n),
+  // column c * hd + x (cross head c of kt_nc, width x), kt_npad keys per head
+  long kt_n, kt_npad;
+  int kt_nc;
   // REFINE: row r of batch (b1, b2) is candidate slot r of latent i = r / R;
   // its key index is ridx[r] (< 0: empty).  The epilogue rotates by tab[key],
   // dots with qex row i and writes (dot, sum of squares) partials.
@@ -467,6 +472,28 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
               const f32x4 q1 = *(const f32x4*)(qe + hh + u);
 #pragma unroll
               for (int w = 0; w < 4; ++w) dp += v0[u + w] * q0[w] + v1[u + w] * q1[w];
+            }
+          } else if (g.kt_n > 0) {
+            // fragment-tiled keys: 8 consecutive widths (jp is a multiple of 8)
+            // are one 16-byte unit; both pair members of the run
+            const long hk = r / g.kt_n, nk = r - hk * g.kt_n;
+            const long hck = hk * g.kt_nc + pc;
+            TC* e0 = C + ktile_off(hck, nk, jp, g.kt_npad, g.hd);
+            TC* e1 = C + ktile_off(hck, nk, jp + hh, g.kt_npad, g.hd);
+            if (nvalid >= PV && sizeof(TC) == 2) {
+              TC t0[PV], t1[PV];
+#pragma unroll
+              for (int w = 0; w < PV; ++w) {
+                t0[w] = from_f32<TC>(v0[w]);
+                t1[w] = from_f32<TC>(v1[w]);
+              }
+              *(uint4*)e0 = *(const uint4*)t0;
+              *(uint4*)e1 = *(const uint4*)t1;
+            } else {
+              for (int u = 0; u < PV && u < nvalid; ++u) {
+                C[ktile_off(hck, nk, jp + u, g.kt_npad, g.hd)] = from_f32<TC>(v0[u]);
+                C[ktile_off(hck, nk, jp + hh + u, g.kt_npad, g.hd)] = from_f32<TC>(v1[u]);
+              }
             }
           } else {
             TC* d0 = C + r * g.ldc + col0;

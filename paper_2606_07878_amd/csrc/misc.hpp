@@ -154,7 +154,8 @@ __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, 
     }
   }
   __syncthreads();
-  // phase 2: X^T rows, 8 keys per store
+  // phase 2: X^T, 8 keys per store: the fragment-tiled layout of the fp16
+  // cross-attention (xtile_off, ldxt keys per head), or row-major [h][f][ldxt]
   const int runs = RW / 8;
   for (int e = threadIdx.x; e < d2 * runs; e += 256) {
     const int f = e / runs, c8 = e - f * runs;
@@ -163,7 +164,8 @@ __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, 
     float v[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) v[u] = to_f32(tile[(8 * c8 + u) * ld + f]);
-    store8(XT + ((long)h * d2 + f) * ldxt + n, v);
+    if constexpr (sizeof(CT) == 2) store8(XT + xtile_off(h, f, n, ldxt, d2), v);
+    else store8(XT + ((long)h * d2 + f) * ldxt + n, v);
   }
 }
 

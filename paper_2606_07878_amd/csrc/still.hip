@@ -115,7 +115,7 @@ constexpr int XATT_KB = 256;   // keys per block of the fp16 cross-attention ker
 constexpr int XATT_TOPK = 4;   // keys tracked per (latent, wave, lane half) by the fp16 kernel
 constexpr int REFINE_R = 4;    // keys per latent whose logits are recomputed accurately
 // waves of the fp16 cross-attention workgroup for a value width d2 = 2d
-constexpr int xatt_waves(int d2) { return d2 >= 256 ? 8 : 4; }
+constexpr int xatt_waves(int) { return 4; }
 
 // ---------------------------------------------------------------------------
 // Derived dimensions and workspace layout
@@ -296,7 +296,8 @@ static Plan make_plan(const still_config* c, const Dims& m) {
     p.ccount = take(4ul * m.H * m.nc);
   }
   const size_t ubase = off;
-  p.k = take(cs * HN * m.Ec);
+  // k: row-major [H*N][nc*dc] (fp32 mode) or fragment-tiled with Npad keys per head (fp16)
+  p.k = take(cs * (m.fp32 ? HN : (long)m.H * m.Npad) * m.Ec);
   p.partk = take(4ul * HN * m.nc * m.np_c);
   p.rk = take(4ul * HN * m.nc);
   p.opart = take(4ul * m.splits * Ht * m.nc * m.d2);
@@ -375,10 +376,8 @@ static hipError_t launch_attn(const AttnArgs& a, int splits, hipStream_t st) {
   if constexpr (sizeof(CT) == 2) {
     constexpr int TT = D2 <= 256 ? 128 : 64;
     const int ntt = (a.t + TT - 1) / TT;
-    constexpr int NW = xatt_waves(D2);
-    constexpr int QC = NW == 8 ? 128 : 64;    // head width per Q stage (register budget of the K ring)
-    hipLaunchKernelGGL((xattn_f16_kernel<TT, QC, D2, XATT_TOPK, NW>), dim3(ntt * a.H * a.nc * splits), dim3(64 * NW),
-                       0, st, a);
+    static_assert(xatt_waves(D2) == 4, "the fp16 kernel runs 4 waves");
+    hipLaunchKernelGGL((xattn_f16_kernel<TT, D2, XATT_TOPK>), dim3(ntt * a.H * a.nc * splits), dim3(256), 0, st, a);
   } else {
     hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, (D2 > 256 ? 32 : ATT_NB), 32, D2, ATT_TOPK>), grid, dim3(256),
                        0, st, a);
@@ -544,6 +543,11 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.tab_mod = (int)m.N;
         g.part = partk;
         g.ldpart = HN;
+        if (!m.fp32) {   // fragment-tiled keys for the fp16 cross-attention kernel
+          g.kt_n = m.N;
+          g.kt_npad = m.Npad;
+          g.kt_nc = m.nc;
+        }
         HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_KPROJ)));
       }
       HIP_TRY(finalize(partq, Ht, m.nc, wide_c ? m.dc / 256 * 2 : m.np_c, rq));
@@ -565,6 +569,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         a.rk = rk;
         a.xt = XT;
         a.ldxt = m.Npad;
+        a.npad = m.Npad;
         a.opart = (float*)(ws + p.opart);
         a.mpart = (float*)(ws + p.mpart);
         a.lpart = (float*)(ws + p.lpart);
