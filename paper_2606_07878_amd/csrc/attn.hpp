@@ -355,24 +355,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     for (int lt = 0; lt < LT; ++lt) o[f][lt] = zero16();
   // Candidate keys for the logit refinement: each lane keeps, per latent
   // tile, a sorted list of its TOPK largest logits (bucket = wave, lane half)
-  // in the output arrays cval/cidx (only the lane itself touches its list),
-  // and in a register the list's smallest entry.  Keys below the running
+  // in registers, written out once at the end.  Keys below the running
   // maximum minus REFINE_MARGIN can never be selected and are skipped, which
   // makes list updates rare.
-  float th[LT];
+  constexpr int TK = TOPK > 0 ? TOPK : 1;
+  float tv[LT][TK];
+  int ti[LT][TK];
 #pragma unroll
-  for (int lt = 0; lt < LT; ++lt) {
-    th[lt] = -INFINITY;
-    const int lat = t0 + 32 * lt + l32;
-    if (TOPK > 0 && lat < a.t) {
-      const long row = ((long)split * HC + hc) * a.t + lat;
+  for (int lt = 0; lt < LT; ++lt)
 #pragma unroll
-      for (int q = 0; q < (TOPK > 0 ? TOPK : 1); ++q) {
-        a.cval[row * (NBK * TOPK) + (2 * w + lg) * TOPK + q] = -INFINITY;
-        a.cidx[row * (NBK * TOPK) + (2 * w + lg) * TOPK + q] = -1;
-      }
+    for (int q = 0; q < TK; ++q) {
+      tv[lt][q] = -INFINITY;
+      ti[lt][q] = -1;
     }
-  }
 
   // Q chunk staging (rows past t read the last row and are stored as zeros)
   half8 qreg[QV];
@@ -491,15 +486,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int f = 0; f < FT; ++f) xr[i][f] = load_x(f, (n0 >> 4) + i);
 
-    // ---- softmax: logit (log2 units) = S * rk, masked past the range end.  The
-    // logits stay in the accumulators: one pass for the block maxima, one for
-    // the probabilities (the refinement candidates recompute them, rarely).
+    // ---- softmax: logit (log2 units) = S * rk, masked past the range end,
+    // written back over S; one pass for the block maxima, one for the
+    // probabilities
     const float* rkc = rks[rbuf];
     const bool tail = n0 + KB > nend;
-    auto logit = [&](int lt, int kt, int j, float rk) -> float {
-      const float x = s[lt][kt][j] * rk;
-      return (tail && n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3) >= nend) ? -INFINITY : x;
-    };
     float mx[LT], lmx[LT];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) mx[lt] = -INFINITY;
@@ -507,12 +498,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
-        const float4 r4 = *(const float4*)&rkc[KW * w + 32 * kt + 8 * jq + 4 * lg];   // keys of j = 4 jq + u
+        const int kl = KW * w + 32 * kt + 8 * jq + 4 * lg;   // keys of j = 4 jq + u: kl + u
+        const float4 r4 = *(const float4*)&rkc[kl];
         const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
 #pragma unroll
         for (int lt = 0; lt < LT; ++lt)
 #pragma unroll
-          for (int u = 0; u < 4; ++u) mx[lt] = fmaxf(mx[lt], logit(lt, kt, 4 * jq + u, rk[u]));
+          for (int u = 0; u < 4; ++u) {
+            float x = s[lt][kt][4 * jq + u] * rk[u];
+            if (tail) x = (n0 + kl + u < nend) ? x : -INFINITY;
+            s[lt][kt][4 * jq + u] = x;
+            mx[lt] = fmaxf(mx[lt], x);
+          }
       }
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
@@ -536,12 +533,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
         for (int jq = 0; jq < 4; ++jq) {
-          const float4 r4 = *(const float4*)&rkc[KW * w + 32 * kt + 8 * jq + 4 * lg];
-          const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
           half4 pv;
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float p = __builtin_amdgcn_exp2f(logit(lt, kt, 4 * jq + u, rk[u]) - mref);
+            const float p = __builtin_amdgcn_exp2f(s[lt][kt][4 * jq + u] - mref);
             ps += p;
             pv[u] = (f16)p;
           }
@@ -550,43 +545,41 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       ps += __shfl_xor(ps, 32);
       if (lg == 0) red_l[li][w] = ps;
       if constexpr (TOPK > 0) {
-        const float cut0 = m_new - REFINE_MARGIN;
-        if (lmx[lt] > fmaxf(th[lt], cut0) && t0 + li < a.t) {   // rare: update this lane's list
-          const long row = ((long)split * HC + hc) * a.t + t0 + li;
-          float* cv = a.cval + row * (NBK * TOPK) + (2 * w + lg) * TOPK;
-          int* ci = a.cidx + row * (NBK * TOPK) + (2 * w + lg) * TOPK;
-          float tv[TOPK > 0 ? TOPK : 1];
-          int ti[TOPK > 0 ? TOPK : 1];
-#pragma unroll
-          for (int q = 0; q < TOPK; ++q) {
-            tv[q] = cv[q];
-            ti[q] = ci[q];
-          }
+        // Keys above cut enter this lane's list.  Usually none; when some lane
+        // has any, it is nearly always exactly one (its block maximum lmx,
+        // inserted directly); two or more take the general loop.
+        const float cut = fmaxf(tv[lt][TOPK - 1], m_new - REFINE_MARGIN);
+        if (lmx[lt] > cut) {
+          int cnt = 0, id = 0;
 #pragma unroll
           for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
-              float v = logit(lt, kt, j, rkc[KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3)]);
-              if (v > fmaxf(tv[TOPK - 1], cut0)) {
-                int id = n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3);
-#pragma unroll
-                for (int q = 0; q < TOPK; ++q) {
-                  const bool gt = v > tv[q];
-                  const float tq = tv[q];
-                  const int iq = ti[q];
-                  tv[q] = gt ? v : tq;
-                  ti[q] = gt ? id : iq;
-                  v = gt ? tq : v;
-                  id = gt ? iq : id;
-                }
-              }
+              const float v = s[lt][kt][j];
+              cnt += v > cut ? 1 : 0;
+              id = v == lmx[lt] ? n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3) : id;
             }
+          auto insert = [&](float v, int k) {
 #pragma unroll
-          for (int q = 0; q < TOPK; ++q) {
-            cv[q] = tv[q];
-            ci[q] = ti[q];
+            for (int q = 0; q < TOPK; ++q) {
+              const bool gt = v > tv[lt][q];
+              const float tq = tv[lt][q];
+              const int iq = ti[lt][q];
+              tv[lt][q] = gt ? v : tq;
+              ti[lt][q] = gt ? k : iq;
+              v = gt ? tq : v;
+              k = gt ? iq : k;
+            }
+          };
+          if (cnt == 1) {
+            insert(lmx[lt], id);
+          } else {
+            for (int kt = 0; kt < KT; ++kt)
+              for (int j = 0; j < 16; ++j) {
+                const float v = s[lt][kt][j];
+                if (v > fmaxf(tv[lt][TOPK - 1], cut)) insert(v, n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3));
+              }
           }
-          th[lt] = tv[TOPK - 1];
         }
       }
       m_run[lt] = m_new;
@@ -656,6 +649,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     if (w == 0 && lg == 0) {
       a.mpart[row] = m_run[lt];
       a.lpart[row] = l_run[lt];
+    }
+    if constexpr (TOPK > 0) {
+#pragma unroll
+      for (int q = 0; q < TOPK; ++q) {
+        a.cval[row * (NBK * TOPK) + (2 * w + lg) * TOPK + q] = tv[lt][q];
+        a.cidx[row * (NBK * TOPK) + (2 * w + lg) * TOPK + q] = ti[lt][q];
+      }
     }
   }
 }
