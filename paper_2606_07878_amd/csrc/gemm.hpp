@@ -189,6 +189,18 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     const int grp = lr / RG, rr = mt * RG + (lr - grp * RG);
     return rr < Mg ? (long)grp * g.mgstride + rr : -1;
   };
+  // the same row as (group, row within the group); with one group the row
+  // itself.  Row indices fit 32 bits (bounded on the host).
+  auto grow2 = [&](int lr, int& grp, int& rr) -> bool {
+    if (mg == 1) {
+      grp = 0;
+      rr = m0 + lr;
+      return rr < M;
+    }
+    grp = lr / RG;
+    rr = mt * RG + (lr - grp * RG);
+    return rr < Mg;
+  };
 
   // global -> register staging, two sets: loads run two k steps ahead
   frag ra[2][AV], rb[2][BV];
@@ -428,10 +440,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       for (int it = 0; it < 32 * NV / 64; ++it) {
         const int e = lane + 64 * it;
         const int rl = e / NV, vx = (e % NV) * PV;
-        const long r = grow(lbase + rl);
+        int rgrp, rrow;
+        const bool rok = grow2(lbase + rl, rgrp, rrow);
+        const long r = rok ? (long)rgrp * g.mgstride + rrow : -1;
         const int nvalid = N - (P0 + vx);
         float sp = 0.f, dp = 0.f;
-        if (r >= 0 && nvalid > 0) {
+        if (rok && nvalid > 0) {
           float v0[PV], v1[PV];
           const float* s0 = stg + rl * SLD + vx;
 #pragma unroll
@@ -448,10 +462,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
           for (int u = 0; u < PV; ++u) sp += v0[u] * v0[u] + v1[u] * v1[u];
           const int jp = pj0 + vx;
           if (g.tab) {
-            long trow;
+            int trow;
             if constexpr (EPI == EPI_REFINE) trow = rkey[lbase + rl];
-            else trow = r % g.tab_mod;
-            const float2* tp = g.tab + trow * hh + jp;
+            else trow = (mg > 1 && g.mgstride == g.tab_mod) ? rrow : (int)r % g.tab_mod;
+            const float2* tp = g.tab + (long)trow * hh + jp;
 #pragma unroll
             for (int u = 0; u < PV; u += 2) {
               const f32x4 cs = *(const f32x4*)(tp + u);
@@ -476,8 +490,15 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
           } else if (g.kt_n > 0) {
             // fragment-tiled keys: 8 consecutive widths (jp is a multiple of 8)
             // are one 16-byte unit; both pair members of the run
-            const long hk = r / g.kt_n, nk = r - hk * g.kt_n;
-            const long hck = hk * g.kt_nc + pc;
+            int hk, nk;
+            if (mg > 1 && g.mgstride == g.kt_n) {
+              hk = rgrp;
+              nk = rrow;
+            } else {
+              hk = (int)r / (int)g.kt_n;
+              nk = (int)r - hk * (int)g.kt_n;
+            }
+            const long hck = (long)hk * g.kt_nc + pc;
             TC* e0 = C + ktile_off(hck, nk, jp, g.kt_npad, g.hd);
             TC* e1 = C + ktile_off(hck, nk, jp + hh, g.kt_npad, g.hd);
             if (nvalid >= PV && sizeof(TC) == 2) {
@@ -540,7 +561,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
             sp += __shfl_xor(sp, o);
             if constexpr (EPI == EPI_REFINE) dp += __shfl_xor(dp, o);
           }
-          if ((e % NV) == 0 && r >= 0) {
+          if ((e % NV) == 0 && rok) {
             if constexpr (EPI == EPI_REFINE) {
               float2* rp = g.rpart + b1 * g.sR1 + b2 * g.sR2;
               rp[(long)rslot[lbase + rl] * nparts + pidx] = make_float2(dp, sp);
