@@ -496,50 +496,100 @@ struct RefineArgs {
 };
 
 // One wave per output row (h, c, i); lane l owns features [l*VPL, (l+1)*VPL).
+// All loads that do not depend on one another are issued before any result
+// is used: the first split's partial row, every split's (m, l), and the
+// refined keys' indices, fp16-path logits and exact-logit partials; the rows
+// of X of the refined keys follow once their indices are known.
 template <class CT, int VPL>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ opart, const float* __restrict__ mpart,
                                                     const float* __restrict__ lpart, int S, int H, int nc, int t,
                                                     CT* __restrict__ O, RefineArgs ra) {
   constexpr int d2 = 64 * VPL;
+  constexpr int RMAX = 8;   // refined keys per latent handled (the host uses REFINE_R <= RMAX)
   const int lane = threadIdx.x & 63;
   const long row = blockIdx.x * 4L + (threadIdx.x >> 6);   // (h*nc + c)*t + i
   const long HCT = (long)H * nc * t;
   if (row >= HCT) return;   // whole wave
   const int hc = (int)(row / t), i = (int)(row - (long)hc * t);
   const int h = hc / nc, c = hc - h * nc;
-  float M = -INFINITY;
-  for (int s = lane; s < S; s += 64) M = fmaxf(M, mpart[s * HCT + row]);
+  const int f0 = lane * VPL;
+  // split 0's partial row (every split holds a partial for every row)
+  float v0[VPL];
+  {
+    const float* op = opart + row * d2 + f0;
+#pragma unroll
+    for (int u = 0; u < VPL; u += 2) {
+      const float2 v = *(const float2*)(op + u);
+      v0[u] = v.x;
+      v0[u + 1] = v.y;
+    }
+  }
+  float ms_l = -INFINITY, ls_l = 0.f;   // this lane's split (lane < S; more splits loop below)
+  if (lane < S) {
+    ms_l = mpart[lane * HCT + row];
+    ls_l = lpart[lane * HCT + row];
+  }
+  int key = -1;
+  float rv = 0.f, dot = 0.f, ss = 0.f;
+  if (lane < ra.R) {
+    key = ra.ridx[row * ra.R + lane];
+    rv = ra.rval[row * ra.R + lane];
+    const float2* p = ra.rpart + (row * ra.R + lane) * ra.NP;
+    float d1 = 0.f, s1 = 0.f;
+    int k = 0;
+    for (; k + 1 < ra.NP; k += 2) {
+      const float2 a = p[k], b = p[k + 1];
+      dot += a.x;
+      ss += a.y;
+      d1 += b.x;
+      s1 += b.y;
+    }
+    if (k < ra.NP) {
+      dot += p[k].x;
+      ss += p[k].y;
+    }
+    dot += d1;
+    ss += s1;
+  }
+  const float rqv = ra.R > 0 ? ra.rq[((long)h * t + i) * nc + c] : 0.f;
+  // maximum and normaliser over the splits
+  float M = ms_l;
+  for (int s = lane + 64; s < S; s += 64) M = fmaxf(M, mpart[s * HCT + row]);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-  float L = 0.f;
-  for (int s = lane; s < S; s += 64) {
+  float L = ms_l != -INFINITY ? exp2f(ms_l - M) * ls_l : 0.f;
+  for (int s = lane + 64; s < S; s += 64) {
     const float ms = mpart[s * HCT + row];
     if (ms != -INFINITY) L += exp2f(ms - M) * lpart[s * HCT + row];
   }
   // weight change of each refined key: 2^(exact - M) - 2^(fp16 - M)
   float dl = 0.f;
-  int key = -1;
-  if (lane < ra.R) {
-    key = ra.ridx[row * ra.R + lane];
-    if (key >= 0) {
-      const float2* p = ra.rpart + (row * ra.R + lane) * ra.NP;
-      float dot = 0.f, ss = 0.f;
-      for (int k = 0; k < ra.NP; ++k) {
-        dot += p[k].x;
-        ss += p[k].y;
-      }
-      const float sx = ra.scale_log2 * ra.rq[((long)h * t + i) * nc + c] * dot / fmaxf(sqrtf(ss), ra.l2_eps);
-      dl = exp2f(sx - M) - exp2f(ra.rval[row * ra.R + lane] - M);
-    }
+  if (lane < ra.R && key >= 0) {
+    const float sx = ra.scale_log2 * rqv * dot / fmaxf(sqrtf(ss), ra.l2_eps);
+    dl = exp2f(sx - M) - exp2f(rv - M);
   }
   L += dl;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
-  const int f0 = lane * VPL;
-  float acc[VPL];
+  // refined keys' rows of X (issued together)
+  float xr[RMAX][VPL];
+  float dr[RMAX];
 #pragma unroll
-  for (int u = 0; u < VPL; ++u) acc[u] = 0.f;
-  for (int s = 0; s < S; ++s) {
+  for (int r = 0; r < RMAX; ++r) {
+    const int n = __shfl(key, r);
+    dr[r] = __shfl(dl, r);
+    const bool use = r < ra.R && n >= 0;
+    const CT* x = (const CT*)ra.X + ((long)h * ra.N + (use ? n : 0)) * d2 + f0;
+#pragma unroll
+    for (int u = 0; u < VPL; ++u) xr[r][u] = use ? to_f32(x[u]) : 0.f;
+    if (!use) dr[r] = 0.f;
+  }
+  const float w0 = __shfl(ms_l, 0);
+  float acc[VPL];
+  const float ws0 = w0 != -INFINITY ? exp2f(w0 - M) : 0.f;
+#pragma unroll
+  for (int u = 0; u < VPL; ++u) acc[u] = ws0 * v0[u];
+  for (int s = 1; s < S; ++s) {
     const float ms = mpart[s * HCT + row];
     if (ms == -INFINITY) continue;
     const float ws = exp2f(ms - M);
@@ -551,14 +601,10 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
       acc[u + 1] += ws * v.y;
     }
   }
-  for (int r = 0; r < ra.R; ++r) {
-    const int n = __shfl(key, r);
-    const float dr = __shfl(dl, r);
-    if (n < 0) continue;
-    const CT* x = (const CT*)ra.X + ((long)h * ra.N + n) * d2 + f0;
 #pragma unroll
-    for (int u = 0; u < VPL; ++u) acc[u] += dr * to_f32(x[u]);
-  }
+  for (int r = 0; r < RMAX; ++r)
+#pragma unroll
+    for (int u = 0; u < VPL; ++u) acc[u] += dr[r] * xr[r][u];
   const float invL = 1.f / L;
   CT* dst = O + ((long)h * t + i) * ((long)nc * d2) + (long)c * d2 + f0;
 #pragma unroll

@@ -114,6 +114,7 @@ constexpr int ATT_TOPK = 4;    // keys tracked per latent half-lane for logit re
 constexpr int XATT_KB = 256;   // keys per block of the fp16 cross-attention kernel
 constexpr int XATT_TOPK = 4;   // keys tracked per (latent, wave, lane half) by the fp16 kernel
 constexpr int REFINE_R = 4;    // keys per latent whose logits are recomputed accurately
+static_assert(REFINE_R <= 8, "merge_kernel handles up to 8 refined keys per latent");
 // waves of the fp16 cross-attention workgroup for a value width d2 = 2d
 constexpr int xatt_waves(int) { return 4; }
 
@@ -341,7 +342,13 @@ constexpr int GEMM_LONG_K = 512;
 template <class CT, class TA, class TB, class TC, class TBias, int EPI, bool WIDE = false>
 static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st, int cls = STILL_K_LATENT) {
   timing::Scope ts(cls, st);
-  if constexpr (WIDE && sizeof(CT) == 2) return launch_gemm<CT, TA, TB, TC, TBias, EPI, 128, 256, 32>(g, batch, st);
+  if constexpr (WIDE && sizeof(CT) == 2) {
+    // 128x256 tiles where they still leave at least two workgroups per CU
+    constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
+    const long ntn = PAIRED ? (g.N + 127) / 128 : (g.N + 255) / 256;
+    const long ntm = g.mgroups > 1 ? (g.M / g.mgroups + 128 / g.mgroups - 1) / (128 / g.mgroups) : (g.M + 127) / 128;
+    if (ntn * ntm * batch >= 512) return launch_gemm<CT, TA, TB, TC, TBias, EPI, 128, 256, 32>(g, batch, st);
+  }
   if (g.K >= GEMM_LONG_K)
     return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
   return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
