@@ -57,11 +57,10 @@ struct GemmArgs {
   float* part;         // PAIR: sum-of-squares partials [head*nparts + p][ldpart] (ldpart >= rows), NULL = none
   long ldpart;
   float* C2;           // PAIR: optional fp32 copy of the (rotated) outputs, ldc as C
-  // PAIR: with kt_n > 0, C is written in the fragment-tiled key layout of the
-  // fp16 cross-attention (ktile_off): row r = h * kt_n + n (KV head h, key n),
-  // column c * hd + x (cross head c of kt_nc, width x), kt_npad keys per head
-  long kt_n, kt_npad;
-  int kt_nc;
+  // PAIR: with qperm, C (not C2) holds each head's widths in the permuted
+  // order of the fp16 cross-attention within every step of 16 (position p of
+  // a step holds width kperm_width(p)); requires hd % 16 == 0
+  int qperm;
   // REFINE: row r of batch (b1, b2) is candidate slot r of latent i = r / R;
   // its key index is ridx[r] (< 0: empty).  The epilogue rotates by tab[key],
   // dots with qex row i and writes (dot, sum of squares) partials.
@@ -487,55 +486,47 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
               for (int w = 0; w < 4; ++w) dp += v0[u + w] * q0[w] + v1[u + w] * q1[w];
             }
-          } else if (g.kt_n > 0) {
-            // fragment-tiled keys: 8 consecutive widths (jp is a multiple of 8)
-            // are one 16-byte unit; both pair members of the run
-            int hk, nk;
-            if (mg > 1 && g.mgstride == g.kt_n) {
-              hk = rgrp;
-              nk = rrow;
-            } else {
-              hk = (int)r / (int)g.kt_n;
-              nk = (int)r - hk * (int)g.kt_n;
-            }
-            const long hck = (long)hk * g.kt_nc + pc;
-            TC* e0 = C + ktile_off(hck, nk, jp, g.kt_npad, g.hd);
-            TC* e1 = C + ktile_off(hck, nk, jp + hh, g.kt_npad, g.hd);
-            if (nvalid >= PV && sizeof(TC) == 2) {
-              TC t0[PV], t1[PV];
-#pragma unroll
-              for (int w = 0; w < PV; ++w) {
-                t0[w] = from_f32<TC>(v0[w]);
-                t1[w] = from_f32<TC>(v1[w]);
-              }
-              *(uint4*)e0 = *(const uint4*)t0;
-              *(uint4*)e1 = *(const uint4*)t1;
-            } else {
-              for (int u = 0; u < PV && u < nvalid; ++u) {
-                C[ktile_off(hck, nk, jp + u, g.kt_npad, g.hd)] = from_f32<TC>(v0[u]);
-                C[ktile_off(hck, nk, jp + hh + u, g.kt_npad, g.hd)] = from_f32<TC>(v1[u]);
-              }
-            }
           } else {
             TC* d0 = C + r * g.ldc + col0;
             constexpr int VE = Vec16<TC>::n;
             const bool vec_ok = nvalid >= PV && (g.ldc % VE) == 0 && (((uintptr_t)C & 15) == 0);
+            float s0[PV], s1[PV];   // values in store order
+#pragma unroll
+            for (int u = 0; u < PV; ++u) {
+              s0[u] = v0[u];
+              s1[u] = v1[u];
+            }
+            if (g.qperm) {
+              // runs jp and jp ^ 8 (lanes e, e ^ 1 of the same row) swap half
+              // runs: the even run stores widths {0-3, 8-11}, the odd one
+              // {4-7, 12-15} of their step of 16
+              const bool even = ((jp >> 3) & 1) == 0;
+#pragma unroll
+              for (int u = 0; u < 4; ++u) {
+                const float r0 = __shfl_xor(even ? v0[4 + u] : v0[u], 1);
+                const float r1 = __shfl_xor(even ? v1[4 + u] : v1[u], 1);
+                s0[u] = even ? v0[u] : r0;
+                s0[4 + u] = even ? r0 : v0[4 + u];
+                s1[u] = even ? v1[u] : r1;
+                s1[4 + u] = even ? r1 : v1[4 + u];
+              }
+            }
             if (vec_ok) {
 #pragma unroll
               for (int u = 0; u < PV; u += VE) {
                 TC t0[VE], t1[VE];
 #pragma unroll
                 for (int w = 0; w < VE; ++w) {
-                  t0[w] = from_f32<TC>(v0[u + w]);
-                  t1[w] = from_f32<TC>(v1[u + w]);
+                  t0[w] = from_f32<TC>(s0[u + w]);
+                  t1[w] = from_f32<TC>(s1[u + w]);
                 }
                 *(uint4*)(d0 + u) = *(const uint4*)t0;
                 *(uint4*)(d0 + hh + u) = *(const uint4*)t1;
               }
             } else {
               for (int u = 0; u < PV && u < nvalid; ++u) {
-                d0[u] = from_f32<TC>(v0[u]);
-                d0[hh + u] = from_f32<TC>(v1[u]);
+                d0[u] = from_f32<TC>(s0[u]);
+                d0[hh + u] = from_f32<TC>(s1[u]);
               }
             }
             if (g.C2) {

@@ -17,6 +17,7 @@
 #include "common.hpp"
 #include "consumer.hpp"
 #include "gemm.hpp"
+#include "kproj.hpp"
 #include "misc.hpp"
 
 namespace still {
@@ -137,6 +138,7 @@ struct Dims {
 struct Plan {
   size_t pq, tab_ck, tab_cq, tab_bk, tab_bq;
   size_t wconv;          // bf16 mode: the layer's weight matrices converted to fp16
+  size_t wkt;            // bf16 mode: fragment-tiled fp16 copy of the cross-attention W_K
   size_t X, XT, Z, Y, q, partq, rq, O;
   size_t Ylo, qex, cval, cidx, ridx, rval, Xc, rpart, crow, ccount;   // logit refinement
   // union region: cross-attention key side ...
@@ -197,6 +199,7 @@ static still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims*
   // the fp16 cross-attention addresses one head's q, k and X^T with 32-bit offsets
   if ((double)N * m->nc * m->dc * 2.0 >= 4294967296.0 || (double)t * m->nc * m->dc * 2.0 >= 4294967296.0)
     return fail(STILL_E_UNSUPPORTED, "N or t too large for one head's 4 GiB key/query span");
+  if (!m->fp32 && m->H > 128) return fail(STILL_E_UNSUPPORTED, "n_kv_heads %d > 128 unsupported", m->H);
   if ((long)m->H * N > (long)GEMM_BN * 65535L)
     return fail(STILL_E_UNSUPPORTED, "H*N = %lld exceeds the supported %ld rows", (long long)(m->H * N), (long)GEMM_BN * 65535L);
   m->tpad = (int)rup(t, 64);
@@ -273,6 +276,7 @@ static Plan make_plan(const still_config* c, const Dims& m) {
   p.tab_bk = take(8ul * m.N * (m.d / 2));
   p.tab_bq = take(8ul * m.t * (m.d / 2));
   p.wconv = m.fp32 ? 0 : take(2ul * matrix_elems(c, m));
+  p.wkt = m.fp32 ? 0 : take(2ul * m.Ec * m.d2);
   p.X = take(cs * HN * m.d2);
   p.XT = take(cs * (size_t)m.H * m.d2 * m.Npad);
   p.Z = take(4ul * Ht * m.D);
@@ -533,12 +537,52 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.hd = m.dc;
         g.tab = tab_cq;
         g.tab_mod = m.t;
+        g.qperm = m.fp32 ? 0 : 1;   // widths in the order of the tiled keys (kproj.hpp)
         g.part = partq;
         g.ldpart = Ht;
         if (wide_c) HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR, true>(g, 1, st, STILL_K_QPROJ)));
         else HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_QPROJ)));
       }
-      {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
+      if constexpr (sizeof(CT) == 2) {
+        // k = RoPE_c(k~), k~ = X W_K^T + b_K, fused kernel writing the tiled key
+        // layout; one sum-of-squares partial per (row, cross head)
+        TIMED(STILL_K_KPROJ);
+        f16* wkt = (f16*)(ws + p.wkt);
+        hipLaunchKernelGGL(tile_w_kernel, dim3(grid1d((long)m.Ec * m.d2 / 8)), dim3(256), 0, st,
+                           (const f16*)bw.ca_wk, (long)m.Ec, m.d2, wkt);
+        HIP_TRY(hipGetLastError());
+        KprojArgs ka;
+        ka.X = (const f16*)X;
+        ka.wkt = wkt;
+        ka.bias = bw.ca_bk;
+        ka.tab = tab_ck;
+        ka.k = (f16*)k;
+        ka.part = partk;
+        ka.H = m.H;
+        ka.N = (int)m.N;
+        ka.nc = m.nc;
+        ka.dc = m.dc;
+        ka.npad = m.Npad;
+        // table stage capacity 16, 64 or 128 key positions (LDS <= 160 KB)
+        ka.kpw = 128 / m.H;
+        const dim3 grid((unsigned)((m.N + ka.kpw - 1) / ka.kpw));
+        if (ka.kpw <= 16) {
+          if (m.d2 == 128) hipLaunchKernelGGL((kproj_kernel<128, 16, IT>), grid, dim3(256), 0, st, ka);
+          else if (m.d2 == 256) hipLaunchKernelGGL((kproj_kernel<256, 16, IT>), grid, dim3(256), 0, st, ka);
+          else hipLaunchKernelGGL((kproj_kernel<512, 16, IT>), grid, dim3(256), 0, st, ka);
+        } else if (ka.kpw <= 64 || m.d2 == 512) {
+          ka.kpw = std::min(ka.kpw, m.d2 == 512 ? 32 : 64);
+          const dim3 g2((unsigned)((m.N + ka.kpw - 1) / ka.kpw));
+          if (m.d2 == 128) hipLaunchKernelGGL((kproj_kernel<128, 64, IT>), g2, dim3(256), 0, st, ka);
+          else if (m.d2 == 256) hipLaunchKernelGGL((kproj_kernel<256, 64, IT>), g2, dim3(256), 0, st, ka);
+          else hipLaunchKernelGGL((kproj_kernel<512, 32, IT>), g2, dim3(256), 0, st, ka);
+        } else {
+          if (m.d2 == 128) hipLaunchKernelGGL((kproj_kernel<128, 128, IT>), grid, dim3(256), 0, st, ka);
+          else hipLaunchKernelGGL((kproj_kernel<256, 128, IT>), grid, dim3(256), 0, st, ka);
+        }
+        HIP_TRY(hipGetLastError());
+        HIP_TRY(finalize(partk, HN, m.nc, 1, rk));
+      } else {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
         GemmArgs g = gargs((int)HN, m.Ec / 2, m.d2, X, m.d2, bw.ca_wk, m.d2, k, m.Ec);
         if (Tile<CT>::BM % m.H == 0) {   // tiles span the same keys of every KV head: shared table rows
           g.mgroups = m.H;
@@ -550,15 +594,10 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
         g.tab_mod = (int)m.N;
         g.part = partk;
         g.ldpart = HN;
-        if (!m.fp32) {   // fragment-tiled keys for the fp16 cross-attention kernel
-          g.kt_n = m.N;
-          g.kt_npad = m.Npad;
-          g.kt_nc = m.nc;
-        }
         HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st, STILL_K_KPROJ)));
+        HIP_TRY(finalize(partk, HN, m.nc, m.np_c, rk));
       }
       HIP_TRY(finalize(partq, Ht, m.nc, wide_c ? m.dc / 256 * 2 : m.np_c, rq));
-      HIP_TRY(finalize(partk, HN, m.nc, m.np_c, rk));
       const float ca_scale = cfg->logit_scale_cross != 0.f ? cfg->logit_scale_cross : (float)m.dc;
       if constexpr (sizeof(CT) == 2) {   // fold 1/||q~|| * scale * log2(e) into q for the fp16 kernel
         TIMED(STILL_K_OTHER);
