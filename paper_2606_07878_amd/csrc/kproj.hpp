@@ -166,7 +166,25 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
           }
         }
         // ---- epilogue: bias, sum of squares, rotation, fp16, tiled stores
-        const TBias* bc = bias ? bias + (long)c * a.dc + 32 * p + 4 * g : nullptr;
+        // biases of this lane's widths: 4 consecutive values per group q (8-byte loads)
+        static_assert(sizeof(TBias) == 2, "2-byte bias type");
+        uint2 bl[4], bu[4];
+        if (bias) {
+          const TBias* bc = bias + (long)c * a.dc + 32 * p + 4 * g;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            bl[q] = *(const uint2*)(bc + 8 * q);
+            bu[q] = *(const uint2*)(bc + hh + 8 * q);
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) bl[q] = bu[q] = make_uint2(0, 0);
+        }
+        auto bias_at = [&](const uint2& v, int u) -> float {
+          const uint32_t wd = u < 2 ? v.x : v.y;
+          const TBias e = __builtin_bit_cast(TBias, (uint16_t)((u & 1) ? (wd >> 16) : (wd & 0xffffu)));
+          return to_f32(e);
+        };
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
           const int pos = kn[kt] - n0;
@@ -182,7 +200,7 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
               const int j = 4 * q + u;
-              const float blo = bc ? to_f32(bc[8 * q + u]) : 0.f, bhi = bc ? to_f32(bc[hh + 8 * q + u]) : 0.f;
+              const float blo = bias_at(bl[q], u), bhi = bias_at(bu[q], u);
               const float ylo = acc[0][kt][j] + blo, yhi = acc[1][kt][j] + bhi;
               ss += ylo * ylo + yhi * yhi;
               olo[j >> 3][j & 7] = (f16)(ylo * cs[u] - yhi * sn[u]);
@@ -198,8 +216,10 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
               const long flo = ((hck * (a.npad >> 5) + (kn[kt] >> 5)) * (a.dc >> 4) + 2 * p + s) << 9;
               const long fhi = flo + ((long)(hh >> 4) << 9);
               const long slot = ((kn[kt] & 31) + 32 * g) * 8;
-              *(half8*)(a.k + flo + slot) = olo[s];
-              *(half8*)(a.k + fhi + slot) = ohi[s];
+              // streaming stores: the keys are read back only by the next
+              // kernel; W_K and the X rows stay in L2
+              __builtin_nontemporal_store(olo[s], (half8*)(a.k + flo + slot));
+              __builtin_nontemporal_store(ohi[s], (half8*)(a.k + fhi + slot));
             }
           }
         }
