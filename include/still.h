@@ -60,6 +60,12 @@ typedef enum {
   STILL_E_HIP = -6           /* a HIP runtime call failed (see still_last_error) */
 } still_status;
 
+/* Shapes the kernels take (anything else the paper allows returns
+ * STILL_E_UNSUPPORTED): head_dim 64, 128 or 256; cross- and self-attention
+ * head widths multiples of 128; latent_dim and ffn_hidden multiples of 8;
+ * N * n_cross_heads * cross width * 2 and t * n_cross_heads * cross width * 2
+ * below 2^32; H * N at most 128 * 65535; in bf16 mode at most 128 KV heads. */
+
 typedef enum { STILL_MODE_BF16 = 0, STILL_MODE_FP32 = 1 } still_mode;
 typedef enum { STILL_FFN_NONE = 0, STILL_FFN_SWIGLU = 1, STILL_FFN_GELU = 2 } still_ffn;
 

@@ -113,8 +113,12 @@ template <> struct VecLoad<float, float> {
 // coalesced 1 KB read.  Lane l of a fragment holds row l % 32 and contraction
 // indices 8 * (l / 32) + [0, 8) of the fragment's 16.
 //   k (projected keys) of KV head h, cross head c (hc = h * nc + c), key n,
-//   width index x (npad keys per head, a multiple of 256):
+//   storage position x (npad keys per head, a multiple of 256):
 //     [hc][n / 32][x / 16][lane = n % 32 + 32 * ((x / 8) % 2)][x % 8]
+//   Position x of a width step of 16 need not hold width x: the key
+//   projection stores its accumulator registers in place, so the query and
+//   the key side agree on one permutation of the 16 widths of each step (the
+//   contraction over the step does not depend on the order).
 //   X^T of KV head h, feature f, key n:
 //     [h][f / 32][n / 16][lane = f % 32 + 32 * ((n / 8) % 2)][n % 8]
 // ---------------------------------------------------------------------------
