@@ -19,6 +19,7 @@
 #include "gemm.hpp"
 #include "kproj.hpp"
 #include "misc.hpp"
+#include "refine.hpp"
 
 namespace still {
 
@@ -295,8 +296,8 @@ static Plan make_plan(const still_config* c, const Dims& m) {
     p.cidx = take(4ul * m.splits * HCT * m.ncand);
     p.ridx = take(4ul * HCT * m.R);
     p.rval = take(4ul * HCT * m.R);
-    p.Xc = take(cs * HCT * m.R * (m.fp32 ? 2 : 3) * m.d);
-    p.rpart = take(8ul * HCT * m.R * (m.dc / 64));
+    p.Xc = m.fp32 ? take(cs * HCT * m.R * 2 * m.d) : 0;   // fp16: rows gathered inside the refine kernel
+    p.rpart = take(8ul * HCT * m.R * (m.fp32 ? m.dc / 64 : 1));
     p.crow = take(4ul * HCT * m.R);
     p.ccount = take(4ul * m.H * m.nc);
   }
@@ -654,18 +655,46 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
             int* ccount = (int*)(ws + p.ccount);
             hipLaunchKernelGGL(refine_compact_kernel, dim3(NB), dim3(256), 0, st, ridx, TR, crow, ccount);
             HIP_TRY(hipGetLastError());
-            hipLaunchKernelGGL((refine_gather_kernel<IT, CT>), dim3(grid1d(HCT * m.R * (m.d / 2))), dim3(256), 0,
-                               st, (const IT*)Kp, (const IT*)Vp, tab_bk, ridx, crow, ccount, m.N, m.d, m.nc, TR, NB,
-                               (CT*)(ws + p.Xc));
-            HIP_TRY(hipGetLastError());
+            if constexpr (SPLIT) {   // fp16: gather, exact key projection and dot product in one kernel
+              RefineKArgs rk_;
+              rk_.K = Kp;
+              rk_.V = Vp;
+              rk_.tab_b = tab_bk;
+              rk_.tab_c = tab_ck;
+              rk_.wkt = (const f16*)(ws + p.wkt);
+              rk_.bias = bw.ca_bk;
+              rk_.ridx = ridx;
+              rk_.crow = crow;
+              rk_.count = ccount;
+              rk_.qex = (const float*)(ws + p.qex);
+              rk_.rpart = (float2*)(ws + p.rpart);
+              rk_.N = m.N;
+              rk_.t = m.t;
+              rk_.R = m.R;
+              rk_.nc = m.nc;
+              rk_.dc = m.dc;
+              constexpr int BMR = 64;   // candidate rows per workgroup (LDS: BMR x 3d fp16; 2-3 workgroups per CU)
+              rk_.H = m.H;
+              rk_.ntile = (TR + BMR - 1) / BMR;
+              const dim3 rg((unsigned)(rk_.ntile * NB));
+              if (m.d == 64) hipLaunchKernelGGL((refine_kernel<64, BMR, IT, IT>), rg, dim3(256), 0, st, rk_);
+              else if (m.d == 128) hipLaunchKernelGGL((refine_kernel<128, BMR, IT, IT>), rg, dim3(256), 0, st, rk_);
+              else hipLaunchKernelGGL((refine_kernel<256, BMR, IT, IT>), rg, dim3(256), 0, st, rk_);
+              HIP_TRY(hipGetLastError());
+            } else {
+              hipLaunchKernelGGL((refine_gather_kernel<IT, CT>), dim3(grid1d(HCT * m.R * (m.d / 2))), dim3(256), 0,
+                                 st, (const IT*)Kp, (const IT*)Vp, tab_bk, ridx, crow, ccount, m.N, m.d, m.nc, TR, NB,
+                                 (CT*)(ws + p.Xc));
+              HIP_TRY(hipGetLastError());
+            }
           }
-          {  // exact k~ of the packed keys: [K_hi | V | K_lo] [W_K | W_K(key half)]^T, dotted with q~
+          if constexpr (!SPLIT) {  // fp32: exact k~ of the packed keys [K | V] [W_K]^T, dotted with q~
             GemmArgs g = gargs(m.t * m.R, m.dc / 2, W, ws + p.Xc, W, bw.ca_wk, m.d2, nullptr, 0);
             g.nb2 = m.nc;
             g.sA1 = (long)m.nc * m.t * m.R * W;
             g.sA2 = (long)m.t * m.R * W;
             g.sB2 = (long)m.dc * m.d2;
-            g.bwrap = SPLIT ? m.d2 : 0;
+            g.bwrap = 0;
             g.bias = bw.ca_bk;
             g.sBias2 = m.dc;
             g.hd = m.dc;
@@ -676,7 +705,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
             g.sI1 = (long)m.nc * m.t * m.R;
             g.sI2 = (long)m.t * m.R;
             g.R = m.R;
-            g.qex = SPLIT ? (const float*)(ws + p.qex) : (const float*)q;   // fp32 mode: q is exact fp32
+            g.qex = (const float*)q;   // fp32 mode: q is exact fp32
             g.ldqex = m.Ec;
             g.sE1 = (long)m.t * m.Ec;
             g.sE2 = m.dc;
@@ -686,7 +715,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
             HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_REFINE>(g, m.H * m.nc, st, STILL_K_REFINE)));
           }
           ra.R = m.R;
-          ra.NP = m.dc / 64;
+          ra.NP = SPLIT ? 1 : m.dc / 64;
           ra.ridx = ridx;
           ra.rval = (const float*)(ws + p.rval);
           ra.rpart = (const float2*)(ws + p.rpart);
