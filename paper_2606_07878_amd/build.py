@@ -9,7 +9,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libstill.so")
 SOURCES = [os.path.join(PKG, "csrc", "still.hip")]
-HEADERS = [os.path.join(PKG, "csrc", f) for f in ("common.hpp", "gemm.hpp", "attn.hpp", "misc.hpp", "kproj.hpp", "consumer.hpp")] + \
+HEADERS = [os.path.join(PKG, "csrc", f) for f in ("common.hpp", "gemm.hpp", "attn.hpp", "misc.hpp", "kproj.hpp", "consumer.hpp", "refine.hpp")] + \
           [os.path.join(ROOT, "include", "still.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

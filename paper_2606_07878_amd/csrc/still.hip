@@ -342,17 +342,17 @@ constexpr int GEMM_LONG_K = 512;
 
 // WIDE: 128 x 256 tiles (BK 32, 2 waves per SIMD) for the latent-side
 // products with many output columns and K >= 512 (fp16 mode; paired kinds need
-// head widths that are multiples of 256).  The norm partials of a PAIR product
-// then number hd/256*2 per head instead of hd/128*2.
+// head widths that are multiples of 256), where they still leave at least two
+// workgroups per CU.  The norm partials of a PAIR product then number hd/256*2
+// per head instead of hd/128*2, so paired kinds always take them.
 template <class CT, class TA, class TB, class TC, class TBias, int EPI, bool WIDE = false>
 static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st, int cls = STILL_K_LATENT) {
   timing::Scope ts(cls, st);
   if constexpr (WIDE && sizeof(CT) == 2) {
-    // 128x256 tiles where they still leave at least two workgroups per CU
     constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
     const long ntn = PAIRED ? (g.N + 127) / 128 : (g.N + 255) / 256;
     const long ntm = g.mgroups > 1 ? (g.M / g.mgroups + 128 / g.mgroups - 1) / (128 / g.mgroups) : (g.M + 127) / 128;
-    if (ntn * ntm * batch >= 512) return launch_gemm<CT, TA, TB, TC, TBias, EPI, 128, 256, 32>(g, batch, st);
+    if (PAIRED || ntn * ntm * batch >= 512) return launch_gemm<CT, TA, TB, TC, TBias, EPI, 128, 256, 32>(g, batch, st);
   }
   if (g.K >= GEMM_LONG_K)
     return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
