@@ -290,8 +290,10 @@ namespace still {
 //       deep: the slot used now is reloaded with the same step of the next
 //       chunk (of the next block, in a block's last chunk, so those loads
 //       have the softmax and P.X of the block to arrive).
-//   softmax: logit (log2 units) = S * rk[key]; per-latent block maxima
-//       combined over the 4 waves through LDS; P (fp16) to LDS [lat][key].
+//   softmax: logit (log2 units) = S * rk[key] * qs[lat] with qs = rq * scale
+//       * log2(e) (the query side of the QK-norm and the logit scale: one
+//       factor per lane and latent tile); per-latent block maxima combined
+//       over the 4 waves through LDS; P (fp16) to LDS [lat][key].
 //   P.X: O^T[feat][lat] += X^T[feat][key] P^T[key][lat]; X^T fragments from
 //       the tiled layout through a ring of XR key steps, P from LDS.
 // Keys past the range end (only in its last block) are masked by a select:
@@ -342,11 +344,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const unsigned ksteps = (unsigned)(a.dc >> 4);   // width steps of one key tile
   const unsigned nsteps = (unsigned)(a.npad >> 4); // key steps of one feature tile
 
-  float m_run[LT], l_run[LT];
+  float m_run[LT], l_run[LT], qs[LT];
 #pragma unroll
   for (int lt = 0; lt < LT; ++lt) {
     m_run[lt] = -INFINITY;
     l_run[lt] = 0.f;
+    const int lat = min(t0 + 32 * lt + l32, a.t - 1);   // rows past t: any positive factor
+    qs[lt] = a.rq[((long)h * a.t + lat) * a.nc + c] * a.scale_log2;
   }
   f32x16 o[FT][LT];
 #pragma unroll
@@ -486,8 +490,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int f = 0; f < FT; ++f) xr[i][f] = load_x(f, (n0 >> 4) + i);
 
-    // ---- softmax: logit (log2 units) = S * rk, masked past the range end,
-    // written back over S; one pass for the block maxima, one for the
+    // ---- softmax: x = S * rk, masked past the range end, written back over
+    // S; logit (log2 units) = x * qs[lt] (qs > 0, so block maxima of x scale
+    // to those of the logits); one pass for the block maxima, one for the
     // probabilities
     const float* rkc = rks[rbuf];
     const bool tail = n0 + KB > nend;
@@ -515,7 +520,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     for (int lt = 0; lt < LT; ++lt) {
       lmx[lt] = mx[lt];
       mx[lt] = fmaxf(mx[lt], __shfl_xor(mx[lt], 32));
-      if (lg == 0) red_m[32 * lt + l32][w] = mx[lt];
+      if (lg == 0) red_m[32 * lt + l32][w] = mx[lt] * qs[lt];
     }
     __syncthreads();
     float alpha[LT];
@@ -536,7 +541,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
           half4 pv;
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float p = __builtin_amdgcn_exp2f(s[lt][kt][4 * jq + u] - mref);
+            const float p = __builtin_amdgcn_exp2f(fmaf(s[lt][kt][4 * jq + u], qs[lt], -mref));
             ps += p;
             pv[u] = (f16)p;
           }
@@ -545,18 +550,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       ps += __shfl_xor(ps, 32);
       if (lg == 0) red_l[li][w] = ps;
       if constexpr (TOPK > 0) {
-        // Keys above cut enter this lane's list.  Usually none; when some lane
-        // has any, it is nearly always exactly one (its block maximum lmx,
-        // inserted directly); two or more take the general loop.
+        // Keys whose logit (x * qs) is above cut enter this lane's list.
+        // Usually none; when some lane has any, it is nearly always exactly
+        // one (its block maximum lmx, inserted directly); two or more take
+        // the general loop.
         const float cut = fmaxf(tv[lt][TOPK - 1], m_new - REFINE_MARGIN);
-        if (lmx[lt] > cut) {
+        if (lmx[lt] * qs[lt] > cut) {
           int cnt = 0, id = 0;
 #pragma unroll
           for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
               const float v = s[lt][kt][j];
-              cnt += v > cut ? 1 : 0;
+              cnt += v * qs[lt] > cut ? 1 : 0;
               id = v == lmx[lt] ? n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3) : id;
             }
           auto insert = [&](float v, int k) {
@@ -572,11 +578,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             }
           };
           if (cnt == 1) {
-            insert(lmx[lt], id);
+            insert(lmx[lt] * qs[lt], id);
           } else {
             for (int kt = 0; kt < KT; ++kt)
               for (int j = 0; j < 16; ++j) {
-                const float v = s[lt][kt][j];
+                const float v = s[lt][kt][j] * qs[lt];
                 if (v > fmaxf(tv[lt][TOPK - 1], cut)) insert(v, n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3));
               }
           }

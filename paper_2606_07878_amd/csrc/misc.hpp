@@ -214,23 +214,6 @@ __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float* __restr
   }
 }
 
-// q[r][c*dc + j] *= rq[r][c] * scale, in place (fp16): folds the query's
-// QK-norm factor and the logit scale into the operand of the QK product.
-__global__ void qprescale_kernel(f16* __restrict__ q, const float* __restrict__ rq, long rows, int nc, int dc,
-                                 float scale) {
-  const long per_row = (long)nc * dc / 8;
-  const long total = rows * per_row;
-  for (long v = blockIdx.x * (long)blockDim.x + threadIdx.x; v < total; v += (long)gridDim.x * blockDim.x) {
-    const long r = v / per_row;
-    const int col = (int)(v - r * per_row) * 8;
-    const float f = rq[r * nc + col / dc] * scale;
-    half8* p = (half8*)(q + r * nc * (long)dc + col);
-    half8 x = *p;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = (f16)((float)x[i] * f);
-    *p = x;
-  }
-}
 
 // rn[r][c] = 1 / max(sqrt(sum_p part[c*np + p][r]), eps)   (QK-norm factors)
 __global__ void finalize_norm_kernel(const float* __restrict__ part, long rows, int nh, int np,

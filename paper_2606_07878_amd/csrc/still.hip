@@ -600,12 +600,6 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
       }
       HIP_TRY(finalize(partq, Ht, m.nc, wide_c ? m.dc / 256 * 2 : m.np_c, rq));
       const float ca_scale = cfg->logit_scale_cross != 0.f ? cfg->logit_scale_cross : (float)m.dc;
-      if constexpr (sizeof(CT) == 2) {   // fold 1/||q~|| * scale * log2(e) into q for the fp16 kernel
-        TIMED(STILL_K_OTHER);
-        hipLaunchKernelGGL(qprescale_kernel, dim3(grid1d(Ht * m.Ec / 8)), dim3(256), 0, st, (f16*)q, rq, Ht, m.nc,
-                           m.dc, ca_scale * LOG2E);
-        HIP_TRY(hipGetLastError());
-      }
       {
         AttnArgs a;
         a.q = q;
