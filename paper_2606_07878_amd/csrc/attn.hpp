@@ -320,6 +320,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   __shared__ __attribute__((aligned(16))) f16 Ps[TT * LP];
   __shared__ float red_m[TT][NW], red_l[TT][NW];
   __shared__ __attribute__((aligned(16))) float rks[2][KB];
+  __shared__ float qsl[TT];   // qs of each latent row (read in the softmax, not held in registers)
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
@@ -344,13 +345,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const unsigned ksteps = (unsigned)(a.dc >> 4);   // width steps of one key tile
   const unsigned nsteps = (unsigned)(a.npad >> 4); // key steps of one feature tile
 
-  float m_run[LT], l_run[LT], qs[LT];
+  float m_run[LT], l_run[LT];
 #pragma unroll
   for (int lt = 0; lt < LT; ++lt) {
     m_run[lt] = -INFINITY;
     l_run[lt] = 0.f;
-    const int lat = min(t0 + 32 * lt + l32, a.t - 1);   // rows past t: any positive factor
-    qs[lt] = a.rq[((long)h * a.t + lat) * a.nc + c] * a.scale_log2;
+  }
+  if (tid < TT) {
+    const int lat = min(t0 + tid, a.t - 1);   // rows past t: any positive factor
+    qsl[tid] = a.rq[((long)h * a.t + lat) * a.nc + c] * a.scale_log2;
   }
   f32x16 o[FT][LT];
 #pragma unroll
@@ -496,7 +499,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // probabilities
     const float* rkc = rks[rbuf];
     const bool tail = n0 + KB > nend;
-    float mx[LT], lmx[LT];
+    float mx[LT], lmx[LT], qs[LT];
+#pragma unroll
+    for (int lt = 0; lt < LT; ++lt) qs[lt] = qsl[32 * lt + l32];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) mx[lt] = -INFINITY;
 #pragma unroll
