@@ -172,8 +172,28 @@ __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, 
 // Z = latents (fp32 residual stream).
 template <class IT>
 __global__ void init_z_kernel(const IT* __restrict__ lat, float* __restrict__ Z, long n) {
-  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
-    Z[i] = to_f32(lat[i]);
+  const long stride = (long)gridDim.x * blockDim.x, i0 = blockIdx.x * (long)blockDim.x + threadIdx.x;
+  if ((n & 7) == 0 && (((uintptr_t)lat | (uintptr_t)Z) & 15) == 0) {   // 8 values per thread and step
+    for (long i = i0; i < n / 8; i += stride) {
+      float v[8];
+      if constexpr (sizeof(IT) == 2) {
+        const uint4 u = *(const uint4*)(lat + 8 * i);
+        const uint32_t wd[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          v[2 * k] = to_f32(__builtin_bit_cast(IT, (uint16_t)(wd[k] & 0xffffu)));
+          v[2 * k + 1] = to_f32(__builtin_bit_cast(IT, (uint16_t)(wd[k] >> 16)));
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) v[k] = to_f32(lat[8 * i + k]);
+      }
+      *(f32x4*)(Z + 8 * i) = f32x4{v[0], v[1], v[2], v[3]};
+      *(f32x4*)(Z + 8 * i + 4) = f32x4{v[4], v[5], v[6], v[7]};
+    }
+  } else {
+    for (long i = i0; i < n; i += stride) Z[i] = to_f32(lat[i]);
+  }
 }
 
 // Y = RMSNorm(Z) per row (non-parametric), one wave per row.

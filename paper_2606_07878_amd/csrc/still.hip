@@ -354,6 +354,17 @@ static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st, int cls = S
     const long ntm = g.mgroups > 1 ? (g.M / g.mgroups + 128 / g.mgroups - 1) / (128 / g.mgroups) : (g.M + 127) / 128;
     if (PAIRED || ntn * ntm * batch >= 512) return launch_gemm<CT, TA, TB, TC, TBias, EPI, 128, 256, 32>(g, batch, st);
   }
+  if constexpr (sizeof(CT) == 2 && EPI != EPI_REFINE) {
+    // fewer 128-row tiles than CUs (the output heads, small t): 64-row tiles
+    constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU);
+    const long ntn = PAIRED ? (g.N + 63) / 64 : (g.N + 127) / 128;
+    const long ntm = g.mgroups > 1 ? (g.M / g.mgroups + 128 / g.mgroups - 1) / (128 / g.mgroups) : (g.M + 127) / 128;
+    if (g.mgroups <= 1 && ntn * ntm * batch < 256) {
+      if (g.K >= GEMM_LONG_K)
+        return launch_gemm<CT, TA, TB, TC, TBias, EPI, 64, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
+      return launch_gemm<CT, TA, TB, TC, TBias, EPI, 64, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
+    }
+  }
   if (g.K >= GEMM_LONG_K)
     return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
   return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
@@ -496,7 +507,7 @@ static still_status run_layer(const still_config* cfg, const Dims& m, const Plan
   }
   {
     TIMED(STILL_K_OTHER);
-    hipLaunchKernelGGL((init_z_kernel<IT>), dim3(grid1d(Ht * m.D)), dim3(256), 0, st, (const IT*)w->latents, Z, Ht * m.D);
+    hipLaunchKernelGGL((init_z_kernel<IT>), dim3(grid1d(Ht * m.D / 8)), dim3(256), 0, st, (const IT*)w->latents, Z, Ht * m.D);
   }
   HIP_TRY(hipGetLastError());
   auto rmsnorm = [&]() -> hipError_t {
