@@ -446,9 +446,10 @@ __global__ __launch_bounds__(256) void refine_compact_kernel(const int* __restri
   if (tid == 255) count[b] = ssum[255];
 }
 
-// Gather the X rows of the packed refinement slots.  fp16 compute: the
-// RoPE-fixed key half is split into high and low parts,
-// Xc[b][j] = [K_hi (d) | V (d) | K_lo (d)]; fp32 compute: Xc[b][j] = [K (d) | V (d)].
+// Gather the X rows of the packed refinement slots for the refinement GEMM of
+// the fp32 path, Xc[b][j] = [K (d) | V (d)] (the fp16 path gathers inside
+// refine_kernel).  With a 2-byte compute type the RoPE-fixed key half is split
+// into high and low parts, Xc[b][j] = [K_hi (d) | V (d) | K_lo (d)].
 template <class IT, class CT>
 __global__ void refine_gather_kernel(const IT* __restrict__ K, const IT* __restrict__ V,
                                      const float2* __restrict__ tab, const int* __restrict__ ridx,
