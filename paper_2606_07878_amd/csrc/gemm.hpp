@@ -130,6 +130,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   static_assert(4 * 32 * SLD * 4 <= LDSB, "staging does not fit");
 
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDSB];
+  __shared__ float sc_f[EPI == EPI_SCALE ? BM + BN : 1];   // SCALE: row factors, then column factors
   CT* As = (CT*)smem;                          // [2][BM*LR]
   CT* Bs = As + 2 * BM * LR;                   // [2][BN*LR]
 
@@ -312,8 +313,34 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     if (kt + 1 < nk) store_stage((kt + 1) & 1, na, nb, nkin);
     __syncthreads();
   };
+  // SCALE: the per-row and per-column factors (BM + BN values) are loaded
+  // together with the first k step's operands and kept in LDS for the
+  // epilogue, so their latency is not exposed after the k loop
+  float scf[(BM + BN + 255) / 256];
+  if constexpr (EPI == EPI_SCALE) {
+    const float* rqv = g.rq + b1 * g.sQ1 + b2 * g.sQ2;
+    const float* rkv = g.rk + b1 * g.sK1 + b2 * g.sK2;
+#pragma unroll
+    for (int i = 0; i < (BM + BN + 255) / 256; ++i) {
+      const int v = tid + 256 * i;
+      float f = 0.f;
+      if (v < BM) {
+        const long r = grow(v);
+        if (r >= 0) f = rqv[r * g.ldrq];
+      } else if (v < BM + BN) {
+        const int col = nt * BN + (v - BM);
+        if (col < N) f = rkv[(long)col * g.ldrk] * g.scale;
+      }
+      scf[i] = f;
+    }
+  }
   kin0 = issue(0, ra[0], rb[0]);
   store_stage(0, ra[0], rb[0], kin0);
+  if constexpr (EPI == EPI_SCALE) {
+#pragma unroll
+    for (int i = 0; i < (BM + BN + 255) / 256; ++i)
+      if (tid + 256 * i < BM + BN) sc_f[tid + 256 * i] = scf[i];
+  }
   kin1 = issue(1, ra[1], rb[1]);
   __syncthreads();
   int kt = 0;
@@ -360,28 +387,18 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     }
     __syncthreads();
   }
-  const float* rqv = (EPI == EPI_SCALE) ? g.rq + b1 * g.sQ1 + b2 * g.sQ2 : nullptr;
-  const float* rkv = (EPI == EPI_SCALE) ? g.rk + b1 * g.sK1 + b2 * g.sK2 : nullptr;
 
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
     const int lbase = wm * (BM / 2) + a * 32;    // tile-local first row of the slice
     // ---- 1. values into the staging slice
     if constexpr (EPI == EPI_SCALE) {
-      // per-column and per-row factors loaded once per slice
-      float rkc[TN];
-#pragma unroll
-      for (int b = 0; b < TN; ++b) {
-        const int col = nt * BN + col_base(b) + l32;
-        rkc[b] = col < N ? rkv[(long)col * g.ldrk] * g.scale : 0.f;
-      }
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
-        const long r = grow(lbase + rl);
-        const float rqs = r >= 0 ? rqv[r * g.ldrq] : 0.f;
 #pragma unroll
-        for (int b = 0; b < TN; ++b) stg[rl * SLD + b * 32 + l32] = acc[a][b][j] * rqs * rkc[b];
+        for (int b = 0; b < TN; ++b)
+          stg[rl * SLD + b * 32 + l32] = acc[a][b][j] * sc_f[lbase + rl] * sc_f[BM + col_base(b) + l32];
       }
     } else if constexpr (!PAIRED) {
 #pragma unroll
