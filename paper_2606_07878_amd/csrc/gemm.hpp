@@ -585,6 +585,47 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       constexpr int VE = Vec16<TC>::n;
       constexpr int VPR = RUN / VE;                  // vectors per run row
       const bool vec_ok = (g.ldc % VE) == 0 && (((uintptr_t)C & 15) == 0);
+      // RESID: C vectors are read in groups of RG before the group's writes
+      // (the compiler cannot move a read of C above an earlier store to C, so
+      // reading in the store loop costs one memory round trip per vector)
+      constexpr int ITN = 32 * NRUN * VPR / 64, RG = 4;
+      if constexpr (EPI == EPI_RESID && (32 * NRUN * VPR) % 64 == 0 && ITN % RG == 0) {
+#pragma unroll
+        for (int g0 = 0; g0 < ITN; g0 += RG) {
+          f32x4 cold[RG];
+          long off[RG];
+          int okv[RG];
+#pragma unroll
+          for (int u = 0; u < RG; ++u) {
+            const int e = lane + 64 * (g0 + u);
+            const int rl = e / (NRUN * VPR);
+            const int rem = e - rl * NRUN * VPR;
+            const int q = rem / VPR, vx = (rem - q * VPR) * VE;
+            const long r = grow(lbase + rl);
+            const long col = run_col(q, vx);
+            off[u] = r < 0 ? -1 : r * g.ldc + col;
+            okv[u] = r < 0 ? 0 : ((N - (int)col >= VE && vec_ok) ? 2 : 1);   // 2: vector, 1: scalar tail
+            if (okv[u] == 2) cold[u] = *(const f32x4*)(C + off[u]);
+          }
+#pragma unroll
+          for (int u = 0; u < RG; ++u) {
+            const int e = lane + 64 * (g0 + u);
+            const int rl = e / (NRUN * VPR);
+            const int rem = e - rl * NRUN * VPR;
+            const int q = rem / VPR, vx = (rem - q * VPR) * VE;
+            const float* src = stg + rl * SLD + q * RUN + vx;
+            if (okv[u] == 2) {
+              f32x4 o = cold[u];
+#pragma unroll
+              for (int w = 0; w < 4; ++w) o[w] += src[w];
+              *(f32x4*)(C + off[u]) = o;
+            } else if (okv[u] == 1) {
+              const int nvalid = N - (int)run_col(q, vx);
+              for (int w = 0; w < VE && w < nvalid; ++w) C[off[u] + w] = from_f32<TC>(to_f32(C[off[u] + w]) + src[w]);
+            }
+          }
+        }
+      } else
       for (int e = lane; e < 32 * NRUN * VPR; e += 64) {
         const int rl = e / (NRUN * VPR);
         const int rem = e - rl * NRUN * VPR;
