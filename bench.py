@@ -5,11 +5,17 @@ One step = one still_compact_model call over every layer of the workload (the
 whole hot path: RoPE-fix staging, cross-attention, self-attention, FFN, output
 heads, re-rotation) with inputs already resident in HBM.  Prints one JSON line.
 
+The headline workload is the 36-layer Qwen-8B-shaped 8k -> 1024 stack; the
+128k -> 655 (200x) stack follows by default under "workloads", measured the
+same way after the headline's buffers are freed.
+
 The dominant kernel (flash cross-attention) is timed live with hipEvent pairs
 on its launch stream during the timed region; its algorithmic FLOPs per launch
 (QK^T and P.X for all KV heads x cross heads of one layer) divided by the
-average launch duration gives the roofline point.  The fp64 oracle is timed
-on a bounded sample (KV heads of one layer, about 25 s) as a CPU baseline.
+average launch duration gives the roofline point.  The KV-stream kernel
+(RoPE-fix staging, the one HBM-bound step) is timed the same way against the
+HBM peak.  The fp64 oracle is timed on a bounded sample (KV heads of one
+layer, about 25 s per workload) as a CPU baseline.
 """
 from __future__ import annotations
 
@@ -175,32 +181,27 @@ def consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding, reps: int = 20, suffix: int
     return res
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", type=int, default=2, help="registered workload id (default: 8k/8x Qwen-8B stack)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-probe-mib", type=int, default=0,
-                    help="run one plain device copy of this many MiB first (HBM counter calibration)")
-    ap.add_argument("--consumer-only", action="store_true",
-                    help="time only the decode attention over the compacted and the full cache (after one "
-                         "compaction step) and print that object")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the compactor forward runs on a "
-              "single MI355X in this build.", file=sys.stderr)
-        sys.exit(2)
+def kv_stream_bytes(w, N=None) -> dict:
+    """Bytes of the RoPE-fix staging kernel per layer: the KV cache read once
+    (the algorithmic stream) and the fp16 X / X^T copies it writes."""
+    c = w.cfg
+    N = N or w.n_tokens
+    npad = -(-N // 256) * 256
+    read = 2 * c.n_kv_heads * N * c.head_dim * 2
+    write = c.n_kv_heads * N * 2 * c.head_dim * 2 + c.n_kv_heads * 2 * c.head_dim * npad * 2
+    return {"read": read, "write": write}
 
+
+def run_workload(wid: int, steps: int, warmup: int, dev, binding, consumer: bool = False) -> dict:
+    """Generate a workload's stack on the device, time `steps` whole steps
+    after `warmup` untimed ones, and return its measurements.  The dominant
+    kernel (cross-attention) and the KV-stream kernel (RoPE-fix staging) are
+    timed live with hipEvent pairs on their launch stream inside the timed
+    region."""
     import torch
-    from paper_2606_07878_amd import binding, configs, synth
+    from paper_2606_07878_amd import configs, synth
 
-    w = configs.get_workload(args.workload)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    if args.copy_probe_mib:
-        copy_probe(args.copy_probe_mib, dev)
+    w = configs.get_workload(wid)
     L = w.n_layers
     print(f"[bench] generating {L} layers of {w.name}", file=sys.stderr, flush=True)
     Ks, Vs, Ws = [], [], []
@@ -261,57 +262,55 @@ def main():
             Pr[r][:t].copy_(outp)
             call(Kr[r], Vr[r], Pr[r], t + Fr)
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         step()
         torch.cuda.synchronize()
-        print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
-    if args.consumer_only:
-        print(json.dumps({"consumer_attend": consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding),
-                          "config": {"workload": w.name}}), flush=True)
-        return
+        print(f"[bench] warmup {i + 1}/{warmup} done", file=sys.stderr, flush=True)
+    kc = binding.KERNEL_CLASSES
     binding.still_timing_reset()
-    binding.still_timing_enable(1 << binding.KERNEL_CLASSES["cross_attn"])
+    binding.still_timing_enable((1 << kc["cross_attn"]) | (1 << kc["stage"]))
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record(stream)
-    for i in range(args.steps):
+    for i in range(steps):
         step()
     e1.record(stream)
     torch.cuda.synchronize()
     binding.still_timing_enable(0)
-    ms_step = e0.elapsed_time(e1) / args.steps
-    att_ms, att_n = binding.still_timing_read(binding.KERNEL_CLASSES["cross_attn"])
-    print(f"[bench] {args.steps} steps, {ms_step:.2f} ms/step", file=sys.stderr, flush=True)
+    ms_step = e0.elapsed_time(e1) / steps
+    att_ms, att_n = binding.still_timing_read(kc["cross_attn"])
+    stg_ms, stg_n = binding.still_timing_read(kc["stage"])
+    print(f"[bench] {w.name}: {steps} steps, {ms_step:.2f} ms/step", file=sys.stderr, flush=True)
 
     # per-class breakdown (separate, untimed pass)
     binding.still_timing_reset()
-    binding.still_timing_enable((1 << len(binding.KERNEL_CLASSES)) - 1)
+    binding.still_timing_enable((1 << len(kc)) - 1)
     step()
     torch.cuda.synchronize()
     binding.still_timing_enable(0)
     breakdown = {}
-    for name, cls in binding.KERNEL_CLASSES.items():
+    for name, cls in kc.items():
         ms, n = binding.still_timing_read(cls)
         if n:
             breakdown[name] = round(ms / L, 4)
     binding.still_timing_reset()
 
-    consumer = consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding)
+    cons = consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding) if consumer else None
 
     tokens_in = N + R * (t + Fr)                        # cache tokens entering the calls of one step
     tokens_per_s_layer = tokens_in * L / (ms_step / 1e3)
     avg_att_s = att_ms / att_n / 1e3
     launch_flops = (ca_flops_per_launch(w) + R * ca_flops_per_launch(w, t + Fr)) / (1 + R)
     achieved = launch_flops / avg_att_s / 1e12
-    out = {
-        "metric": "cache tokens compacted/sec/layer + % HBM BW or % MFMA peak, 1 MI355X",
+    kvb = [kv_stream_bytes(w)] + [kv_stream_bytes(w, t + Fr)] * R
+    kv_read = sum(b["read"] for b in kvb) / len(kvb)
+    kv_moved = sum(b["read"] + b["write"] for b in kvb) / len(kvb)
+    avg_stg_s = stg_ms / stg_n / 1e3
+    res = {
         "value": round(tokens_per_s_layer, 1),
-        "unit": "tokens/s/layer",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 3),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f16", "data": "synthetic",
+        "ms_per_layer": round(ms_step / L, 4),
         "config": {"workload": w.name, "layers": L, "N": N, "t": t, "rounds": R, "fresh_per_round": Fr,
                    "H_kv": w.cfg.n_kv_heads,
                    "d": w.cfg.head_dim, "D": w.cfg.latent_dim, "n_cross": w.cfg.n_cross_heads,
@@ -319,18 +318,86 @@ def main():
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "mfma", "kernel": "cross_attn", "achieved": round(achieved, 2),
                      "peak": PEAK_FP16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP16_TFLOPS, 4),
-                     "traffic": measured_traffic(args.workload), "traffic_unit": "bytes/launch",
+                     "traffic": measured_traffic(wid), "traffic_unit": "bytes/launch",
                      "avg_launch_ms": round(avg_att_s * 1e3, 4),
                      "launches": att_n,
                      "flops_per_launch": launch_flops},
+        "kv_stream": {"bound": "hbm", "kernel": "stage_x (RoPE-fix staging)", "unit": "GB/s",
+                      "peak": PEAK_HBM_GBS, "avg_launch_ms": round(avg_stg_s * 1e3, 4), "launches": stg_n,
+                      "algorithmic_bytes": kv_read, "achieved": round(kv_read / avg_stg_s / 1e9, 1),
+                      "frac": round(kv_read / avg_stg_s / 1e9 / PEAK_HBM_GBS, 4),
+                      "moved_bytes": kv_moved, "moved_GB_s": round(kv_moved / avg_stg_s / 1e9, 1),
+                      "moved_frac": round(kv_moved / avg_stg_s / 1e9 / PEAK_HBM_GBS, 4)},
         "layer_mfma_frac": round((layer_flops(w) + R * layer_flops(w, t + Fr)) / (ms_step / L / 1e3) / 1e12
                                  / PEAK_FP16_TFLOPS, 4),
         "kernel_ms_per_layer": breakdown,
-        "consumer_attend": consumer,
     }
+    if cons is not None:
+        res["consumer_attend"] = cons
+    del Ks, Vs, Ws, ws, Ck, Cv, Kr, Vr, Pr
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=2, help="registered workload id (default: 8k/8x Qwen-8B stack)")
+    ap.add_argument("--extra-workloads", default="4",
+                    help="comma-separated workload ids also measured after the headline one, each reported "
+                         "under 'workloads' (default: 4, the 128k/200x stack; '' for none)")
+    ap.add_argument("--extra-steps", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (HBM counter calibration)")
+    ap.add_argument("--consumer-only", action="store_true",
+                    help="time only the decode attention over the compacted and the full cache (after one "
+                         "compaction step) and print that object")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the compactor forward runs on a "
+              "single MI355X in this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_07878_amd import binding, configs
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib, dev)
+    if args.consumer_only:
+        w = configs.get_workload(args.workload)
+        res = run_workload(args.workload, 1, args.warmup, dev, binding, consumer=True)
+        print(json.dumps({"consumer_attend": res["consumer_attend"], "config": {"workload": w.name}}), flush=True)
+        return
+    head = run_workload(args.workload, args.steps, args.warmup, dev, binding, consumer=True)
+    extras = [int(x) for x in args.extra_workloads.split(",") if x.strip() and int(x) != args.workload]
+    workloads = {}
+    for wid in extras:
+        r = run_workload(wid, args.extra_steps, 1, dev, binding)
+        r.update({"steps": args.extra_steps, "warmup": 1, "unit": "tokens/s/layer"})
+        workloads[f"workload_{wid}"] = r
+    out = {
+        "metric": "cache tokens compacted/sec/layer + % HBM BW or % MFMA peak, 1 MI355X",
+        "value": head["value"],
+        "unit": "tokens/s/layer",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16", "data": "synthetic",
+    }
+    out.update({k: v for k, v in head.items() if k not in ("value", "ms_per_step")})
+    if workloads:
+        out["workloads"] = workloads
     if not args.no_cpu_baseline:
-        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w)
+        print("[bench] timing the CPU oracle on bounded samples", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(configs.get_workload(args.workload))
+        for wid in extras:
+            out["workloads"][f"workload_{wid}"]["cpu_baseline"] = cpu_baseline(configs.get_workload(wid))
     print(json.dumps(out), flush=True)
 
 

@@ -249,9 +249,10 @@ enum {
   STILL_K_QPROJ = 2,        /* cross-attention query projection               */
   STILL_K_REFINE = 3,       /* exact-logit refinement of the top keys         */
   STILL_K_LATENT = 4,       /* latent-side GEMMs (V/O proj, self-attn, FFN, heads) */
-  STILL_K_OTHER = 5,        /* staging, norms, softmax, merge, tables, beta    */
+  STILL_K_OTHER = 5,        /* norms, softmax, merge, tables, conversions, beta */
   STILL_K_ATTEND = 6,       /* still_attend: consumer attention and its merge  */
-  STILL_K_COUNT = 7
+  STILL_K_STAGE = 7,        /* RoPE-fix staging of X, X^T: the KV-cache stream */
+  STILL_K_COUNT = 8
 };
 still_status still_timing_enable(int32_t class_mask);
 still_status still_timing_reset(void);

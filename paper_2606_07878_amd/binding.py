@@ -214,7 +214,8 @@ def still_version() -> str:
 
 
 # kernel classes of the timing facility (still.h)
-KERNEL_CLASSES = {"cross_attn": 0, "kproj": 1, "qproj": 2, "refine": 3, "latent": 4, "other": 5, "attend": 6}
+KERNEL_CLASSES = {"cross_attn": 0, "kproj": 1, "qproj": 2, "refine": 3, "latent": 4, "other": 5, "attend": 6,
+                  "stage": 7}
 
 
 def still_timing_enable(class_mask: int) -> None:

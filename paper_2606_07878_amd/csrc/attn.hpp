@@ -36,9 +36,16 @@ struct AttnArgs {
   int H, N, t, nc, dc, d2;
   float scale_log2;  // logit scale * log2(e)
   int keys_per_split;
-  float* cval;       // TOPK > 0: [S][H*nc][t][2*TOPK] largest logits seen (log2 units) ...
-  int* cidx;         // ... and their key indices (-1 = none), per half-lane
+  float* cval;       // TOPK > 0: [S][H*nc][t][ncand] largest logits seen (log2 units) ...
+  int* cidx;         // ... and their key indices (-1 = none), per half-lane; fp16 kernel:
+                     // [0, NBK*TOPK) the per-bucket lists, then up to XATT_OVF overflow entries
+  int* ocnt;         // fp16 kernel: [S][H*nc][t] overflow entries written per row
 };
+
+// Overflow capacity per (split, latent row) of the fp16 kernel: in-margin keys
+// that a full register list rejects or evicts (exact ties of duplicated cache
+// rows, or more near-maximal keys per lane than the list holds).
+constexpr int XATT_OVF = 128;
 
 template <class CT, int TT, int NB, int DK, int D2, int TOPK>
 __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
@@ -178,15 +185,17 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
           if (x > tv[TOPK - 1]) {
             float v = x;
             int id = n0 + kl;
+            bool moved = false;   // entries after the insertion point shift (exact ties too)
 #pragma unroll
             for (int q = 0; q < TOPK; ++q) {
-              const bool gt = v > tv[q];
+              const bool gt = moved || v > tv[q];
               const float tvq = tv[q];
               const int tiq = ti[q];
               tv[q] = gt ? v : tvq;
               ti[q] = gt ? id : tiq;
               v = gt ? tvq : v;
               id = gt ? tiq : id;
+              moved = gt;
             }
           }
         }
@@ -321,6 +330,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   __shared__ float red_m[TT][NW], red_l[TT][NW];
   __shared__ __attribute__((aligned(16))) float rks[2][KB];
   __shared__ float qsl[TT];   // qs of each latent row (read in the softmax, not held in registers)
+  __shared__ int ovn[TT];     // overflow entries of each latent row
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
@@ -354,6 +364,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   if (tid < TT) {
     const int lat = min(t0 + tid, a.t - 1);   // rows past t: any positive factor
     qsl[tid] = a.rq[((long)h * a.t + lat) * a.nc + c] * a.scale_log2;
+    ovn[tid] = 0;
   }
   f32x16 o[FT][LT];
 #pragma unroll
@@ -555,12 +566,49 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       ps += __shfl_xor(ps, 32);
       if (lg == 0) red_l[li][w] = ps;
       if constexpr (TOPK > 0) {
-        // Keys whose logit (x * qs) is above cut enter this lane's list.
-        // Usually none; when some lane has any, it is nearly always exactly
-        // one (its block maximum lmx, inserted directly); two or more take
-        // the general loop.
-        const float cut = fmaxf(tv[lt][TOPK - 1], m_new - REFINE_MARGIN);
-        if (lmx[lt] * qs[lt] > cut) {
+        // Keys whose logit (x * qs) lies within REFINE_MARGIN of the running
+        // maximum are candidates.  Usually a lane has none; when it has
+        // some, it is nearly always exactly one (its block maximum lmx,
+        // handled directly); two or more take the general loop.  A candidate
+        // enters the lane's sorted list if it beats the list's last entry;
+        // the entry it pushes out, or the candidate itself when it does not
+        // enter, goes to the row's overflow list if it is still in the
+        // margin, so no in-margin key is lost while the overflow has room.
+        // Padding rows past t (zero queries: every key ties at logit 0) are
+        // skipped.
+        const float cut = m_new - REFINE_MARGIN;
+        if (t0 + li < a.t && lmx[lt] * qs[lt] > cut) {
+          const long orow = ((long)split * HC + hc) * a.t + (t0 + li);
+          auto overflow = [&](float v, int k) {
+            const int slot = atomicAdd(&ovn[li], 1);
+            if (slot < XATT_OVF) {
+              a.cval[orow * (NBK * TOPK + XATT_OVF) + NBK * TOPK + slot] = v;
+              a.cidx[orow * (NBK * TOPK + XATT_OVF) + NBK * TOPK + slot] = k;
+            }
+          };
+          auto push = [&](float v, int k) {
+            if (!(v > tv[lt][TOPK - 1])) {
+              overflow(v, k);
+              return;
+            }
+            const float ev = tv[lt][TOPK - 1];
+            const int ek = ti[lt][TOPK - 1];
+            // insert before the first smaller entry; every entry after it
+            // shifts down one place (also past equal values: exact ties)
+            bool moved = false;
+#pragma unroll
+            for (int q = 0; q < TOPK; ++q) {
+              const bool gt = moved || v > tv[lt][q];
+              const float tq = tv[lt][q];
+              const int iq = ti[lt][q];
+              tv[lt][q] = gt ? v : tq;
+              ti[lt][q] = gt ? k : iq;
+              v = gt ? tq : v;
+              k = gt ? iq : k;
+              moved = gt;
+            }
+            if (ek >= 0 && ev > cut) overflow(ev, ek);
+          };
           int cnt = 0, id = 0;
 #pragma unroll
           for (int kt = 0; kt < KT; ++kt)
@@ -570,25 +618,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
               cnt += v * qs[lt] > cut ? 1 : 0;
               id = v == lmx[lt] ? n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3) : id;
             }
-          auto insert = [&](float v, int k) {
-#pragma unroll
-            for (int q = 0; q < TOPK; ++q) {
-              const bool gt = v > tv[lt][q];
-              const float tq = tv[lt][q];
-              const int iq = ti[lt][q];
-              tv[lt][q] = gt ? v : tq;
-              ti[lt][q] = gt ? k : iq;
-              v = gt ? tq : v;
-              k = gt ? iq : k;
-            }
-          };
           if (cnt == 1) {
-            insert(lmx[lt] * qs[lt], id);
+            push(lmx[lt] * qs[lt], id);
           } else {
             for (int kt = 0; kt < KT; ++kt)
               for (int j = 0; j < 16; ++j) {
                 const float v = s[lt][kt][j] * qs[lt];
-                if (v > fmaxf(tv[lt][TOPK - 1], cut)) insert(v, n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3));
+                if (v > cut) push(v, n0 + KW * w + 32 * kt + 8 * (j >> 2) + 4 * lg + (j & 3));
               }
           }
         }
@@ -664,9 +700,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     if constexpr (TOPK > 0) {
 #pragma unroll
       for (int q = 0; q < TOPK; ++q) {
-        a.cval[row * (NBK * TOPK) + (2 * w + lg) * TOPK + q] = tv[lt][q];
-        a.cidx[row * (NBK * TOPK) + (2 * w + lg) * TOPK + q] = ti[lt][q];
+        a.cval[row * (NBK * TOPK + XATT_OVF) + (2 * w + lg) * TOPK + q] = tv[lt][q];
+        a.cidx[row * (NBK * TOPK + XATT_OVF) + (2 * w + lg) * TOPK + q] = ti[lt][q];
       }
+      if (w == 0 && lg == 0) a.ocnt[row] = min(ovn[32 * lt + l32], XATT_OVF);
     }
   }
 }

@@ -40,7 +40,7 @@ __host__ __device__ __forceinline__ int kperm_width(int p) {
 
 // W (fp16, row-major [rows][d2]) -> fragment-tiled copy; one thread per
 // 16-byte unit.
-__global__ void tile_w_kernel(const f16* __restrict__ w, long rows, int d2, f16* __restrict__ out) {
+static __global__ void tile_w_kernel(const f16* __restrict__ w, long rows, int d2, f16* __restrict__ out) {
   const long units = rows * (d2 / 8);
   for (long u = blockIdx.x * (long)blockDim.x + threadIdx.x; u < units; u += (long)gridDim.x * blockDim.x) {
     const long row = u / (d2 / 8);

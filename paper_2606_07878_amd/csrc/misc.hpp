@@ -11,7 +11,7 @@ namespace still {
 // Latent / output positions: p_i = p_min + i (p_max - p_min)/(t-1) over the
 // supplied key positions (p_0 = p_min when t = 1).  One workgroup.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void positions_kernel(const double* __restrict__ p, long N, int t,
+static __global__ __launch_bounds__(256) void positions_kernel(const double* __restrict__ p, long N, int t,
                                                         double* __restrict__ pq, double* __restrict__ out) {
   __shared__ double smin[256], smax[256];
   double lo = INFINITY, hi = -INFINITY;
@@ -45,7 +45,7 @@ __global__ __launch_bounds__(256) void positions_kernel(const double* __restrict
 // Angles are formed and reduced in float64 (positions up to ~1e5 times
 // frequencies near 1 need more than float32's 24 bits), then rounded.
 // ---------------------------------------------------------------------------
-__global__ void rope_table_kernel(const double* __restrict__ pos, long R, int w, double base,
+static __global__ void rope_table_kernel(const double* __restrict__ pos, long R, int w, double base,
                                   float2* __restrict__ tab) {
   const int hh = w / 2;
   const long total = R * hh;
@@ -215,7 +215,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ 
 // Y = RMSNorm(Z) split into a high and a low fp16 part (Y ~= hi + lo to
 // about 22 bits) for products whose result must be more accurate than one
 // fp16 rounding of Y allows.
-__global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float* __restrict__ Z, f16* __restrict__ Yhi,
+static __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float* __restrict__ Z, f16* __restrict__ Yhi,
                                                             f16* __restrict__ Ylo, long rows, int D, float eps) {
   const long row = blockIdx.x * 4L + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -236,7 +236,7 @@ __global__ __launch_bounds__(256) void rmsnorm_split_kernel(const float* __restr
 
 
 // rn[r][c] = 1 / max(sqrt(sum_p part[c*np + p][r]), eps)   (QK-norm factors)
-__global__ void finalize_norm_kernel(const float* __restrict__ part, long rows, int nh, int np,
+static __global__ void finalize_norm_kernel(const float* __restrict__ part, long rows, int nh, int np,
                                      float eps, float* __restrict__ rn) {
   const long total = rows * nh;
   for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
@@ -379,58 +379,93 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* __restri
 // 2^-REFINE_MARGIN of the row maximum.
 // ---------------------------------------------------------------------------
 
-// Pick, per latent row, the R largest fp16 logits among the flash pass's
-// per-split candidates that lie within REFINE_MARGIN of the row maximum.
-__global__ void refine_select_kernel(const float* __restrict__ cval, const int* __restrict__ cidx,
-                                     const float* __restrict__ mpart, int S, long HCT, int C, int R,
-                                     int* __restrict__ ridx, float* __restrict__ rval) {
-  const long row = blockIdx.x * (long)blockDim.x + threadIdx.x;
-  if (row >= HCT) return;
+// Pick, per latent row, every candidate of the flash pass's per-split lists
+// whose logit lies within REFINE_MARGIN of the row maximum, largest first, up
+// to R of them: slots [0, rcnt[row]) of the row hold them.  Exact ties (duplicated
+// cache rows) are all taken, so their weights stay consistent.  A split's
+// list of C entries holds CB fixed entries, then (with ocnt) ocnt[split][row]
+// overflow entries.
+//
+// One wave per row: the lists are read with coalesced loads, the in-margin
+// candidates (usually two or three) are compacted into LDS, and each takes
+// its rank among them, equal logits ordered by key index, so the selection
+// does not depend on the order in which the flash pass appended overflow
+// entries.
+template <int R>
+__global__ __launch_bounds__(256) void refine_select_kernel(const float* __restrict__ cval,
+                                                            const int* __restrict__ cidx,
+                                                            const int* __restrict__ ocnt,
+                                                            const float* __restrict__ mpart, int S, long HCT, int C,
+                                                            int CB, int* __restrict__ ridx, float* __restrict__ rval,
+                                                            int* __restrict__ rcnt) {
+  constexpr int CAP = 256;   // in-margin candidates kept per row
+  __shared__ float sv[4][CAP];
+  __shared__ int si[4][CAP];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const long row = blockIdx.x * 4L + wv;
+  const bool active = row < HCT;
   float M = -INFINITY;
-  for (int s = 0; s < S; ++s) M = fmaxf(M, mpart[s * HCT + row]);
-  float bv[8];
-  int bi[8];
-  for (int q = 0; q < R; ++q) {
-    bv[q] = -INFINITY;
-    bi[q] = -1;
-  }
-  for (int s = 0; s < S; ++s) {
-    const float* cv = cval + (s * HCT + row) * C;
-    const int* ci = cidx + (s * HCT + row) * C;
-    for (int k = 0; k < C; ++k) {
-      float v = cv[k];
-      int id = ci[k];
-      if (id < 0 || !(v >= M - REFINE_MARGIN) || !(v > bv[R - 1])) continue;
-      for (int q = 0; q < R; ++q) {
-        if (v > bv[q]) {
-          const float tv = bv[q];
-          const int tid = bi[q];
-          bv[q] = v;
-          bi[q] = id;
-          v = tv;
-          id = tid;
+  if (active)
+    for (int s = lane; s < S; s += 64) M = fmaxf(M, mpart[s * HCT + row]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  const float cut = M - REFINE_MARGIN;
+  int n = 0;
+  if (active) {
+    for (int s = 0; s < S; ++s) {
+      const long base = (s * HCT + row) * C;
+      const int cnt = CB + (ocnt ? ocnt[s * HCT + row] : 0);
+      for (int k0 = 0; k0 < cnt; k0 += 64) {
+        const int k = k0 + lane;
+        float v = -INFINITY;
+        int id = -1;
+        if (k < cnt) {
+          v = cval[base + k];
+          id = cidx[base + k];
         }
+        const bool keep = id >= 0 && v >= cut;
+        const unsigned long long mask = __ballot(keep);
+        const int pos = n + __popcll(mask & ((1ull << lane) - 1ull));
+        if (keep && pos < CAP) {
+          sv[wv][pos] = v;
+          si[wv][pos] = id;
+        }
+        n += __popcll(mask);
       }
     }
   }
-  for (int q = 0; q < R; ++q) {
-    ridx[row * R + q] = bi[q];
-    rval[row * R + q] = bv[q];
+  n = min(n, CAP);
+  __syncthreads();
+  if (!active) return;
+  for (int j = lane; j < n; j += 64) {
+    const float v = sv[wv][j];
+    const int id = si[wv][j];
+    int rank = 0;
+    for (int q = 0; q < n; ++q) {
+      const float vq = sv[wv][q];
+      const int iq = si[wv][q];
+      rank += (vq > v || (vq == v && iq < id)) ? 1 : 0;
+    }
+    if (rank < R) {
+      ridx[row * R + rank] = id;
+      rval[row * R + rank] = v;
+    }
   }
+  if (lane == 0) rcnt[row] = min(n, R);
 }
 
-// Pack the non-empty refinement slots of each (KV head, cross head): for
-// batch b, crow[b][0..count[b]) lists the slots (index into the b's t*R slots)
-// whose key is >= 0, in slot order.  One workgroup per batch.
-__global__ __launch_bounds__(256) void refine_compact_kernel(const int* __restrict__ ridx, int TR,
+// Pack the refinement slots of each (KV head, cross head) list b: crow[b][j],
+// j < count[b], lists the slots (latent i, rank q < rcnt[b][i]) as i * R + q,
+// in slot order.  One workgroup per list.
+static __global__ __launch_bounds__(256) void refine_compact_kernel(const int* __restrict__ rcnt, int t, int R,
                                                              int* __restrict__ crow, int* __restrict__ count) {
   __shared__ int ssum[256];
   const int b = blockIdx.x, tid = threadIdx.x;
-  const int per = (TR + 255) / 256;
-  const int lo = min(TR, tid * per), hi = min(TR, lo + per);
-  const int* rb = ridx + (long)b * TR;
+  const int per = (t + 255) / 256;
+  const int lo = min(t, tid * per), hi = min(t, lo + per);
+  const int* rc = rcnt + (long)b * t;
   int n = 0;
-  for (int i = lo; i < hi; ++i) n += rb[i] >= 0;
+  for (int i = lo; i < hi; ++i) n += rc[i];
   ssum[tid] = n;
   __syncthreads();
   for (int o = 1; o < 256; o <<= 1) {   // inclusive scan
@@ -440,59 +475,29 @@ __global__ __launch_bounds__(256) void refine_compact_kernel(const int* __restri
     __syncthreads();
   }
   int pos = ssum[tid] - n;
-  int* cb = crow + (long)b * TR;
-  for (int i = lo; i < hi; ++i)
-    if (rb[i] >= 0) cb[pos++] = i;
-  if (tid == 255) count[b] = ssum[255];
-}
-
-// Gather the X rows of the packed refinement slots for the refinement GEMM of
-// the fp32 path, Xc[b][j] = [K (d) | V (d)] (the fp16 path gathers inside
-// refine_kernel).  With a 2-byte compute type the RoPE-fixed key half is split
-// into high and low parts, Xc[b][j] = [K_hi (d) | V (d) | K_lo (d)].
-template <class IT, class CT>
-__global__ void refine_gather_kernel(const IT* __restrict__ K, const IT* __restrict__ V,
-                                     const float2* __restrict__ tab, const int* __restrict__ ridx,
-                                     const int* __restrict__ crow, const int* __restrict__ count, long N, int d,
-                                     int nc, int TR, int nbatch, CT* __restrict__ Xc) {
-  constexpr bool SPLIT = sizeof(CT) == 2;
-  const int hh = d / 2, W = SPLIT ? 3 * d : 2 * d;
-  const long total = (long)nbatch * TR * hh;
-  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total; e += (long)gridDim.x * blockDim.x) {
-    const long row = e / hh;                 // b * TR + j
-    const int j = (int)(e - row * hh);
-    const int b = (int)(row / TR), jr = (int)(row - (long)b * TR);
-    if (jr >= count[b]) continue;
-    const int h = b / nc;
-    const int slot = crow[row];
-    const int n = ridx[(long)b * TR + slot];
-    CT* x = Xc + row * W;
-    const IT* kr = K + ((long)h * N + n) * d;
-    const IT* vr = V + ((long)h * N + n) * d;
-    const float2 cs = tab[(long)n * hh + j];
-    const float a = to_f32(kr[j]), bb = to_f32(kr[j + hh]);
-    const float y0 = a * cs.x + bb * cs.y, y1 = bb * cs.x - a * cs.y;
-    const CT h0 = (CT)y0, h1 = (CT)y1;
-    x[j] = h0;
-    x[j + hh] = h1;
-    if (SPLIT) {
-      x[2 * d + j] = (CT)(y0 - (float)h0);
-      x[2 * d + j + hh] = (CT)(y1 - (float)h1);
-    }
-    x[d + j] = (CT)to_f32(vr[j]);
-    x[d + j + hh] = (CT)to_f32(vr[j + hh]);
+  int* cb = crow + (long)b * t * R;
+  for (int i = lo; i < hi; ++i) {
+    const int ni = rc[i];
+    for (int q = 0; q < ni; ++q) cb[pos++] = i * R + q;
   }
+  if (tid == 255) count[b] = ssum[255];
 }
 
 // Merge split-N partials into O[h*t + i][c*2d + f]:
 //   O = (sum_s 2^(m_s - M) O_s + sum_r D_r X_r) / (sum_s 2^(m_s - M) l_s + sum_r D_r)
-// where, for each refined key r, D_r = 2^(S_exact - M) - 2^(S_fp16 - M) swaps
-// its fp16-logit weight for the accurate one (R = 0: plain merge).
+// where, for each refined key r, D_r = 2^(S_exact - M) - 2^(S_flash - M) swaps
+// the weight the flash pass gave it for the accurate one (R = 0: plain merge).
+// Slots [0, rcnt[row]) of a row hold its refined keys.
+constexpr int REFINE_RMAX = 64;   // refined keys per latent the merge handles (one per lane)
 struct RefineArgs {
   int R, NP;
   const int* ridx;          // [H*nc*t][R]
-  const float* rval;        // [H*nc*t][R]   fp16 logits used by the flash pass (log2 units)
-  const float2* rpart;      // [H*nc*t*R][NP] (dot, sum of squares) partials of the exact keys
+  const int* rcnt;          // [H*nc*t]      refined keys of each row
+  const float* rval;        // [H*nc*t][R]   logits used by the flash pass (log2 units)
+  // NP > 0: [H*nc*t*R][NP] (dot, sum of squares) partials of the exact keys,
+  //         combined here with rq into the exact logit;
+  // NP = 0: [H*nc*t*R] with .x = exact logit - flash logit (fp64 refinement)
+  const float2* rpart;
   const float* rq;          // [H*t][nc]     1 / ||q~||
   const void* X;            // [H*N][2d]     the rows the flash pass multiplied by P
   long N;
@@ -502,14 +507,13 @@ struct RefineArgs {
 // One wave per output row (h, c, i); lane l owns features [l*VPL, (l+1)*VPL).
 // All loads that do not depend on one another are issued before any result
 // is used: the first split's partial row, every split's (m, l), and the
-// refined keys' indices, fp16-path logits and exact-logit partials; the rows
-// of X of the refined keys follow once their indices are known.
+// refined keys' indices, flash logits and exact-logit data; the rows of X of
+// the refined keys follow, four at a time, once their indices are known.
 template <class CT, int VPL>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ opart, const float* __restrict__ mpart,
                                                     const float* __restrict__ lpart, int S, int H, int nc, int t,
                                                     CT* __restrict__ O, RefineArgs ra) {
   constexpr int d2 = 64 * VPL;
-  constexpr int RMAX = 8;   // refined keys per latent handled (the host uses REFINE_R <= RMAX)
   const int lane = threadIdx.x & 63;
   const long row = blockIdx.x * 4L + (threadIdx.x >> 6);   // (h*nc + c)*t + i
   const long HCT = (long)H * nc * t;
@@ -535,27 +539,32 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
   }
   int key = -1;
   float rv = 0.f, dot = 0.f, ss = 0.f;
-  if (lane < ra.R) {
+  const int nref = ra.R > 0 ? ra.rcnt[row] : 0;
+  if (lane < nref) {
     key = ra.ridx[row * ra.R + lane];
     rv = ra.rval[row * ra.R + lane];
-    const float2* p = ra.rpart + (row * ra.R + lane) * ra.NP;
-    float d1 = 0.f, s1 = 0.f;
-    int k = 0;
-    for (; k + 1 < ra.NP; k += 2) {
-      const float2 a = p[k], b = p[k + 1];
-      dot += a.x;
-      ss += a.y;
-      d1 += b.x;
-      s1 += b.y;
+    if (ra.NP == 0) {
+      dot = ra.rpart[row * ra.R + lane].x;
+    } else {
+      const float2* p = ra.rpart + (row * ra.R + lane) * ra.NP;
+      float d1 = 0.f, s1 = 0.f;
+      int k = 0;
+      for (; k + 1 < ra.NP; k += 2) {
+        const float2 a = p[k], b = p[k + 1];
+        dot += a.x;
+        ss += a.y;
+        d1 += b.x;
+        s1 += b.y;
+      }
+      if (k < ra.NP) {
+        dot += p[k].x;
+        ss += p[k].y;
+      }
+      dot += d1;
+      ss += s1;
     }
-    if (k < ra.NP) {
-      dot += p[k].x;
-      ss += p[k].y;
-    }
-    dot += d1;
-    ss += s1;
   }
-  const float rqv = ra.R > 0 ? ra.rq[((long)h * t + i) * nc + c] : 0.f;
+  const float rqv = ra.R > 0 && ra.NP > 0 ? ra.rq[((long)h * t + i) * nc + c] : 0.f;
   // maximum and normaliser over the splits
   float M = ms_l;
   for (int s = lane + 64; s < S; s += 64) M = fmaxf(M, mpart[s * HCT + row]);
@@ -566,33 +575,43 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
     const float ms = mpart[s * HCT + row];
     if (ms != -INFINITY) L += exp2f(ms - M) * lpart[s * HCT + row];
   }
-  // weight change of each refined key: 2^(exact - M) - 2^(fp16 - M)
+  // weight change of each refined key: 2^(exact - M) - 2^(flash - M)
   float dl = 0.f;
-  if (lane < ra.R && key >= 0) {
-    const float sx = ra.scale_log2 * rqv * dot / fmaxf(sqrtf(ss), ra.l2_eps);
-    dl = exp2f(sx - M) - exp2f(rv - M);
+  if (lane < nref) {
+    if (ra.NP == 0) {
+      dl = exp2f(rv - M) * expm1f(dot * 0.69314718055994531f);
+    } else {
+      const float sx = ra.scale_log2 * rqv * dot / fmaxf(sqrtf(ss), ra.l2_eps);
+      dl = exp2f(sx - M) - exp2f(rv - M);
+    }
   }
   L += dl;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
-  // refined keys' rows of X (issued together)
-  float xr[RMAX][VPL];
-  float dr[RMAX];
-#pragma unroll
-  for (int r = 0; r < RMAX; ++r) {
-    const int n = __shfl(key, r);
-    dr[r] = __shfl(dl, r);
-    const bool use = r < ra.R && n >= 0;
-    const CT* x = (const CT*)ra.X + ((long)h * ra.N + (use ? n : 0)) * d2 + f0;
-#pragma unroll
-    for (int u = 0; u < VPL; ++u) xr[r][u] = use ? to_f32(x[u]) : 0.f;
-    if (!use) dr[r] = 0.f;
-  }
   const float w0 = __shfl(ms_l, 0);
   float acc[VPL];
   const float ws0 = w0 != -INFINITY ? exp2f(w0 - M) : 0.f;
 #pragma unroll
   for (int u = 0; u < VPL; ++u) acc[u] = ws0 * v0[u];
+  // refined keys' rows of X, four at a time
+  for (int r0 = 0; r0 < nref; r0 += 4) {
+    float xr[4][VPL];
+    float dr[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int n = __shfl(key, r0 + q);
+      dr[q] = __shfl(dl, r0 + q);
+      const bool use = r0 + q < nref;
+      const CT* x = (const CT*)ra.X + ((long)h * ra.N + (use ? n : 0)) * d2 + f0;
+#pragma unroll
+      for (int u = 0; u < VPL; ++u) xr[q][u] = to_f32(x[u]);
+      if (!use) dr[q] = 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int u = 0; u < VPL; ++u) acc[u] += dr[q] * xr[q][u];
+  }
   for (int s = 1; s < S; ++s) {
     const float ms = mpart[s * HCT + row];
     if (ms == -INFINITY) continue;
@@ -605,10 +624,6 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
       acc[u + 1] += ws * v.y;
     }
   }
-#pragma unroll
-  for (int r = 0; r < RMAX; ++r)
-#pragma unroll
-    for (int u = 0; u < VPL; ++u) acc[u] += dr[r] * xr[r][u];
   const float invL = 1.f / L;
   CT* dst = O + ((long)h * t + i) * ((long)nc * d2) + (long)c * d2 + f0;
 #pragma unroll

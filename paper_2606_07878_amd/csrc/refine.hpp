@@ -40,7 +40,7 @@ struct RefineKArgs {
   float2* rpart;          // [H*nc][t*R] (dot, sum of squares) per slot
   long N;
   int t, R, H, nc, dc;
-  int ntile;              // row tiles per list (the grid holds ntile * H * nc workgroups)
+  int ntile;              // row tiles per list the grid covers (ntile * H * nc workgroups, looping)
 };
 
 // four consecutive I/O values as floats (8-byte load for bf16)
@@ -81,191 +81,197 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
   const int T = gridDim.x;
   int q = blockIdx.x;
   if ((T & 7) == 0) q = (q & 7) * (T >> 3) + (q >> 3);
-  const int rt = q % a.ntile, q2 = q / a.ntile;
+  const int rt0 = q % a.ntile, q2 = q / a.ntile;
   const int h = q2 % a.H, c = q2 / a.H;
   const int b = h * a.nc + c;                     // list (h, c)
-  const int cnt = a.count[b];
-  const int r0 = rt * BM;
-  if (r0 >= cnt) return;                          // uniform
+  const int cnt = a.count[b];                     // uniform
   const int TR = a.t * a.R;
   const int hh = a.dc >> 1;
   const long Ec = (long)a.nc * a.dc;
   const int* crow = a.crow + (long)b * TR;
   const int* ridx = a.ridx + (long)b * TR;
 
-  // ---- gather: row r of the tile = list row r0 + r (zero past the count)
-  for (int r = tid; r < BM; r += 256) {
-    int key = 0, lat = 0;
-    if (r0 + r < cnt) {
-      const int slot = crow[r0 + r];
-      key = max(ridx[slot], 0);
-      lat = slot / a.R;
-    }
-    rinfo[r] = make_int2(key, lat);
-  }
-  __syncthreads();
-  const IT* Kh = (const IT*)a.K + (long)h * a.N * D;
-  const IT* Vh = (const IT*)a.V + (long)h * a.N * D;
-  for (int v = tid; v < BM * (HD / 4); v += 256) {
-    const int r = v / (HD / 4), j = (v - r * (HD / 4)) * 4;   // pairs j .. j + 3
-    const bool ok = r0 + r < cnt;
-    const long n = rinfo[r].x;
-    f16* row = As + r * LA;
-    float k0[4], k1[4], v0[4], v1[4];
-    f32x4 cs01 = {1.f, 0.f, 1.f, 0.f}, cs23 = {1.f, 0.f, 1.f, 0.f};
-#pragma unroll
-    for (int u = 0; u < 4; ++u) k0[u] = k1[u] = v0[u] = v1[u] = 0.f;
-    if (ok) {
-      const IT* kr = Kh + n * D;
-      const IT* vr = Vh + n * D;
-      load4f(kr + j, k0);
-      load4f(kr + j + HD, k1);
-      load4f(vr + j, v0);
-      load4f(vr + j + HD, v1);
-      cs01 = *(const f32x4*)(a.tab_b + n * HD + j);
-      cs23 = *(const f32x4*)(a.tab_b + n * HD + j + 2);
-    }
-    const float cc[4] = {cs01[0], cs01[2], cs23[0], cs23[2]};
-    const float ss[4] = {cs01[1], cs01[3], cs23[1], cs23[3]};
-    half4 h0, h1, l0, l1, w0, w1;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      // un-rotation of the base RoPE (rotate-half pairs j, j + d/2)
-      const float y0 = k0[u] * cc[u] + k1[u] * ss[u];
-      const float y1 = k1[u] * cc[u] - k0[u] * ss[u];
-      h0[u] = (f16)y0;
-      h1[u] = (f16)y1;
-      l0[u] = (f16)(y0 - (float)h0[u]);
-      l1[u] = (f16)(y1 - (float)h1[u]);
-      w0[u] = (f16)v0[u];
-      w1[u] = (f16)v1[u];
-    }
-    *(half4*)&row[j] = h0;
-    *(half4*)&row[j + HD] = h1;
-    *(half4*)&row[D + j] = w0;
-    *(half4*)&row[D + j + HD] = w1;
-    *(half4*)&row[2 * D + j] = l0;
-    *(half4*)&row[2 * D + j + HD] = l1;
-  }
-  __syncthreads();
-
-  // ---- W_K fragments: member m (0: widths p, 1: widths p + dc/2) of this
-  // wave's 32 pairs in column tile ct, k step s
-  const f16* wkc = a.wkt + (long)c * a.dc * (2 * D);
-  const int nct = (hh + PT - 1) / PT;
-  // pairs past dc/2 (last column tile, when PT does not divide dc/2) read the
-  // first tile's rows and are dropped
-  auto ct_ld = [&](int ct) { return (PT * ct + 32 * w < hh) ? ct : 0; };
-  auto load_b = [&](int ct, int m, int s) -> half8 {
-    const int row0 = PT * ct + 32 * w + m * hh;   // multiple of 32
-    const int sk = s < KW ? s : s - KW;
-    return *(const half8*)(wkc + ((((long)(row0 >> 5) * KW + sk) << 9) + 8 * lane));
-  };
-
-  float dps[TC], sps[TC];
-#pragma unroll
-  for (int i = 0; i < TC; ++i) dps[i] = sps[i] = 0.f;
-
-  half8 br[RB][2];
-#pragma unroll
-  for (int s = 0; s < RB; ++s)
-#pragma unroll
-    for (int m = 0; m < 2; ++m) br[s][m] = load_b(ct_ld(0), m, s);
-
-  const f16* Ab = As + l32 * LA + 8 * g;
-  const TBias* bb = a.bias ? (const TBias*)a.bias + (long)c * a.dc : nullptr;
-  const float* qh = a.qex + (long)h * a.t * Ec + (long)c * a.dc;
-  for (int ct = 0; ct < nct; ++ct) {
-    const int ctn = ct_ld(ct + 1 < nct ? ct + 1 : ct);
-    f32x16 acc[TC][2];
-#pragma unroll
-    for (int i = 0; i < TC; ++i) acc[i][0] = acc[i][1] = zero16();
-    half8 af[2][TC];
-#pragma unroll
-    for (int i = 0; i < TC; ++i) af[0][i] = *(const half8*)&Ab[32 * i * LA];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      if (s + 1 < KS) {
-#pragma unroll
-        for (int i = 0; i < TC; ++i) af[(s + 1) & 1][i] = *(const half8*)&Ab[32 * i * LA + 16 * (s + 1)];
+  // The grid covers ntile row tiles of each list; a workgroup takes tiles
+  // rt0, rt0 + ntile, ... while they hold rows.
+  for (int rt = rt0; rt * BM < cnt; rt += a.ntile) {
+    const int r0 = rt * BM;
+    __syncthreads();   // the previous tile's LDS reads are done
+    // ---- gather: row r of the tile = list row r0 + r (zero past the count)
+    for (int r = tid; r < BM; r += 256) {
+      int key = 0, lat = 0;
+      if (r0 + r < cnt) {
+        const int slot = crow[r0 + r];
+        key = max(ridx[slot], 0);
+        lat = slot / a.R;
       }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < TC; ++i)
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-          acc[i][m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(br[s % RB][m], af[s & 1][i], acc[i][m], 0, 0, 0);
-      // refill the ring slot with step s + RB (of the next column tile past the end)
-      const int sn = s + RB;
-#pragma unroll
-      for (int m = 0; m < 2; ++m) br[s % RB][m] = sn < KS ? load_b(ct_ld(ct), m, sn) : load_b(ctn, m, sn - KS);
-      __builtin_amdgcn_sched_barrier(0);
+      rinfo[r] = make_int2(key, lat);
     }
-
-    // ---- epilogue of the column tile: lane holds candidate 32 i + l32 and
-    // pairs p0 + 8 jq + [0, 4) (register j = 4 jq + u)
-    const int p0 = PT * ct + 32 * w + 4 * g;
-    if (PT * ct + 32 * w < hh) {
-      float bs0[16], bs1[16];
+    __syncthreads();
+    const IT* Kh = (const IT*)a.K + (long)h * a.N * D;
+    const IT* Vh = (const IT*)a.V + (long)h * a.N * D;
+    for (int v = tid; v < BM * (HD / 4); v += 256) {
+      const int r = v / (HD / 4), j = (v - r * (HD / 4)) * 4;   // pairs j .. j + 3
+      const bool ok = r0 + r < cnt;
+      const long n = rinfo[r].x;
+      f16* row = As + r * LA;
+      float k0[4], k1[4], v0[4], v1[4];
+      f32x4 cs01 = {1.f, 0.f, 1.f, 0.f}, cs23 = {1.f, 0.f, 1.f, 0.f};
 #pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        float t0[4] = {0.f, 0.f, 0.f, 0.f}, t1[4] = {0.f, 0.f, 0.f, 0.f};
-        if (bb) {
-          load4f(bb + p0 + 8 * jq, t0);
-          load4f(bb + p0 + 8 * jq + hh, t1);
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          bs0[4 * jq + u] = t0[u];
-          bs1[4 * jq + u] = t1[u];
-        }
+      for (int u = 0; u < 4; ++u) k0[u] = k1[u] = v0[u] = v1[u] = 0.f;
+      if (ok) {
+        const IT* kr = Kh + n * D;
+        const IT* vr = Vh + n * D;
+        load4f(kr + j, k0);
+        load4f(kr + j + HD, k1);
+        load4f(vr + j, v0);
+        load4f(vr + j + HD, v1);
+        cs01 = *(const f32x4*)(a.tab_b + n * HD + j);
+        cs23 = *(const f32x4*)(a.tab_b + n * HD + j + 2);
       }
+      const float cc[4] = {cs01[0], cs01[2], cs23[0], cs23[2]};
+      const float ss[4] = {cs01[1], cs01[3], cs23[1], cs23[3]};
+      half4 h0, h1, l0, l1, w0, w1;
 #pragma unroll
-      for (int i = 0; i < TC; ++i) {
-        const int2 ri = rinfo[32 * i + l32];
-        const float2* tr = a.tab_c + (long)ri.x * hh + p0;
-        const float* qr = qh + (long)ri.y * Ec + p0;
-        float dp = 0.f, sp = 0.f;
+      for (int u = 0; u < 4; ++u) {
+        // un-rotation of the base RoPE (rotate-half pairs j, j + d/2)
+        const float y0 = k0[u] * cc[u] + k1[u] * ss[u];
+        const float y1 = k1[u] * cc[u] - k0[u] * ss[u];
+        h0[u] = (f16)y0;
+        h1[u] = (f16)y1;
+        l0[u] = (f16)(y0 - (float)h0[u]);
+        l1[u] = (f16)(y1 - (float)h1[u]);
+        w0[u] = (f16)v0[u];
+        w1[u] = (f16)v1[u];
+      }
+      *(half4*)&row[j] = h0;
+      *(half4*)&row[j + HD] = h1;
+      *(half4*)&row[D + j] = w0;
+      *(half4*)&row[D + j + HD] = w1;
+      *(half4*)&row[2 * D + j] = l0;
+      *(half4*)&row[2 * D + j + HD] = l1;
+    }
+    __syncthreads();
+
+    // ---- W_K fragments: member m (0: widths p, 1: widths p + dc/2) of this
+    // wave's 32 pairs in column tile ct, k step s
+    const f16* wkc = a.wkt + (long)c * a.dc * (2 * D);
+    const int nct = (hh + PT - 1) / PT;
+    // First pair of this wave's 32 in column tile ct.  A wave with no pairs
+    // left there (32 w >= dc/2 in the last tile, e.g. every tile when
+    // dc/2 < PT) loads the head's first 32 pairs instead, so every W_K row it
+    // reads lies inside the head, and its results are dropped.
+    auto ct_ld = [&](int ct) { return (PT * ct + 32 * w < hh) ? PT * ct + 32 * w : 0; };
+    auto load_b = [&](int pbase, int m, int s) -> half8 {
+      const int row0 = pbase + m * hh;   // multiple of 32, row0 + 31 < dc
+      const int sk = s < KW ? s : s - KW;
+      return *(const half8*)(wkc + ((((long)(row0 >> 5) * KW + sk) << 9) + 8 * lane));
+    };
+
+    float dps[TC], sps[TC];
+#pragma unroll
+    for (int i = 0; i < TC; ++i) dps[i] = sps[i] = 0.f;
+
+    half8 br[RB][2];
+#pragma unroll
+    for (int s = 0; s < RB; ++s)
+#pragma unroll
+      for (int m = 0; m < 2; ++m) br[s][m] = load_b(ct_ld(0), m, s);
+
+    const f16* Ab = As + l32 * LA + 8 * g;
+    const TBias* bb = a.bias ? (const TBias*)a.bias + (long)c * a.dc : nullptr;
+    const float* qh = a.qex + (long)h * a.t * Ec + (long)c * a.dc;
+    for (int ct = 0; ct < nct; ++ct) {
+      const int ctn = ct_ld(ct + 1 < nct ? ct + 1 : ct);
+      f32x16 acc[TC][2];
+#pragma unroll
+      for (int i = 0; i < TC; ++i) acc[i][0] = acc[i][1] = zero16();
+      half8 af[2][TC];
+#pragma unroll
+      for (int i = 0; i < TC; ++i) af[0][i] = *(const half8*)&Ab[32 * i * LA];
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        if (s + 1 < KS) {
+#pragma unroll
+          for (int i = 0; i < TC; ++i) af[(s + 1) & 1][i] = *(const half8*)&Ab[32 * i * LA + 16 * (s + 1)];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < TC; ++i)
+#pragma unroll
+          for (int m = 0; m < 2; ++m)
+            acc[i][m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(br[s % RB][m], af[s & 1][i], acc[i][m], 0, 0, 0);
+        // refill the ring slot with step s + RB (of the next column tile past the end)
+        const int sn = s + RB;
+#pragma unroll
+        for (int m = 0; m < 2; ++m) br[s % RB][m] = sn < KS ? load_b(ct_ld(ct), m, sn) : load_b(ctn, m, sn - KS);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+
+      // ---- epilogue of the column tile: lane holds candidate 32 i + l32 and
+      // pairs p0 + 8 jq + [0, 4) (register j = 4 jq + u)
+      const int p0 = PT * ct + 32 * w + 4 * g;
+      if (PT * ct + 32 * w < hh) {
+        float bs0[16], bs1[16];
 #pragma unroll
         for (int jq = 0; jq < 4; ++jq) {
-          const f32x4 q0 = *(const f32x4*)(qr + 8 * jq);
-          const f32x4 q1 = *(const f32x4*)(qr + 8 * jq + hh);
-          const f32x4 c01 = *(const f32x4*)(tr + 8 * jq);
-          const f32x4 c23 = *(const f32x4*)(tr + 8 * jq + 2);
-          const float cc[4] = {c01[0], c01[2], c23[0], c23[2]};
-          const float ss[4] = {c01[1], c01[3], c23[1], c23[3]};
+          float t0[4] = {0.f, 0.f, 0.f, 0.f}, t1[4] = {0.f, 0.f, 0.f, 0.f};
+          if (bb) {
+            load4f(bb + p0 + 8 * jq, t0);
+            load4f(bb + p0 + 8 * jq + hh, t1);
+          }
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const float v0 = acc[i][0][4 * jq + u] + bs0[4 * jq + u];
-            const float v1 = acc[i][1][4 * jq + u] + bs1[4 * jq + u];
-            sp += v0 * v0 + v1 * v1;
-            const float y0 = v0 * cc[u] - v1 * ss[u], y1 = v1 * cc[u] + v0 * ss[u];
-            dp += y0 * q0[u] + y1 * q1[u];
+            bs0[4 * jq + u] = t0[u];
+            bs1[4 * jq + u] = t1[u];
           }
         }
-        dps[i] += dp;
-        sps[i] += sp;
+#pragma unroll
+        for (int i = 0; i < TC; ++i) {
+          const int2 ri = rinfo[32 * i + l32];
+          const float2* tr = a.tab_c + (long)ri.x * hh + p0;
+          const float* qr = qh + (long)ri.y * Ec + p0;
+          float dp = 0.f, sp = 0.f;
+#pragma unroll
+          for (int jq = 0; jq < 4; ++jq) {
+            const f32x4 q0 = *(const f32x4*)(qr + 8 * jq);
+            const f32x4 q1 = *(const f32x4*)(qr + 8 * jq + hh);
+            const f32x4 c01 = *(const f32x4*)(tr + 8 * jq);
+            const f32x4 c23 = *(const f32x4*)(tr + 8 * jq + 2);
+            const float cc[4] = {c01[0], c01[2], c23[0], c23[2]};
+            const float ss[4] = {c01[1], c01[3], c23[1], c23[3]};
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const float v0 = acc[i][0][4 * jq + u] + bs0[4 * jq + u];
+              const float v1 = acc[i][1][4 * jq + u] + bs1[4 * jq + u];
+              sp += v0 * v0 + v1 * v1;
+              const float y0 = v0 * cc[u] - v1 * ss[u], y1 = v1 * cc[u] + v0 * ss[u];
+              dp += y0 * q0[u] + y1 * q1[u];
+            }
+          }
+          dps[i] += dp;
+          sps[i] += sp;
+        }
       }
     }
-  }
 
-  // ---- per-row sums: the two lane halves, then the 4 waves
+    // ---- per-row sums: the two lane halves, then the 4 waves
 #pragma unroll
-  for (int i = 0; i < TC; ++i) {
-    const float dp = dps[i] + __shfl_xor(dps[i], 32);
-    const float sp = sps[i] + __shfl_xor(sps[i], 32);
-    if (g == 0) red[w][32 * i + l32] = make_float2(dp, sp);
-  }
-  __syncthreads();
-  for (int r = tid; r < BM; r += 256) {
-    if (r0 + r >= cnt) continue;
-    float2 s = red[0][r];
-#pragma unroll
-    for (int u = 1; u < 4; ++u) {
-      s.x += red[u][r].x;
-      s.y += red[u][r].y;
+    for (int i = 0; i < TC; ++i) {
+      const float dp = dps[i] + __shfl_xor(dps[i], 32);
+      const float sp = sps[i] + __shfl_xor(sps[i], 32);
+      if (g == 0) red[w][32 * i + l32] = make_float2(dp, sp);
     }
-    a.rpart[(long)b * TR + crow[r0 + r]] = s;
+    __syncthreads();
+    for (int r = tid; r < BM; r += 256) {
+      if (r0 + r >= cnt) continue;
+      float2 s = red[0][r];
+#pragma unroll
+      for (int u = 1; u < 4; ++u) {
+        s.x += red[u][r].x;
+        s.y += red[u][r].y;
+      }
+      a.rpart[(long)b * TR + crow[r0 + r]] = s;
+    }
   }
 }
 

@@ -203,3 +203,23 @@ def test_attend_pointer_and_workspace_checks():
     # NULL beta (no bias) and NULL suffix pointers with n_suffix = 0 pass validation
     c0 = _acfg(n_suffix=0)
     assert _attend(c0, beta=None, k=None, v=None, ws_bytes=16) == -4
+
+
+@pytest.mark.parametrize("dc", [128, 256, 384, 512, 1024, 2048])
+def test_refine_kernel_wk_rows_stay_inside_the_head(dc):
+    """Host model of the W_K fragment rows the fp16 refinement kernel loads
+    (refine.hpp: column tiles of 128 pairs, 32 pairs per wave, both RoPE
+    members dc/2 apart; a wave with no pairs left in a tile loads the head's
+    first 32 pairs).  Every row read must lie inside the cross head's dc rows,
+    so no load reaches past the last head of the tiled W_K."""
+    PT, hh = 128, dc // 2
+    nct = (hh + PT - 1) // PT
+    rows = set()
+    for ct in range(nct):
+        for w in range(4):
+            pbase = PT * ct + 32 * w if PT * ct + 32 * w < hh else 0
+            for m in range(2):
+                row0 = pbase + m * hh
+                rows.update(range(row0, row0 + 32))
+    assert min(rows) >= 0 and max(rows) < dc
+    assert rows == set(range(dc))   # and every row of the head is used

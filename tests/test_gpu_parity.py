@@ -48,14 +48,16 @@ def test_config1_no_rerotate():
 
 
 MULTI_BLOCK_XFAIL = pytest.mark.xfail(
-    reason="B=2 conditioning: a relative input perturbation of 5e-4 (1e-7) moves the exact output by 0.18 "
-           "(7e-5); block-1 residual error of fp16 latent-side products is amplified ~10x by block 2's "
-           "d_l-scaled attention", strict=False)
+    reason="B=2 at the d_l logit scale with bf16 I/O: a relative input perturbation of 5e-4 (fp16 rounding) "
+           "moves the exact output by 0.18; block 1's fp16-operand error in the latent state is amplified "
+           "~10x by block 2's d_l-scaled attention (measured 3.5e-2 - 4.8e-2; the fp32 mode passes)",
+           strict=False)
 
 
 @pytest.mark.parametrize("variant", ["gelu", "final_norm", "no_self", "no_ffn",
                                      pytest.param("two_blocks", marks=MULTI_BLOCK_XFAIL), "resampler", "one_head"])
 def test_config1_variants(variant):
+    """Compactor variants on the cfg-1 cache, bf16 I/O."""
     ch = {"gelu": dict(ffn_kind=configs.FFN_GELU),
           "final_norm": dict(final_norm=1),
           "no_self": dict(n_self_heads=0),
@@ -66,8 +68,7 @@ def test_config1_variants(variant):
     _case(configs.shrink(W1, **ch), name=f"cfg1 {variant}")
 
 
-@MULTI_BLOCK_XFAIL
-@pytest.mark.parametrize("mode", [configs.MODE_BF16, configs.MODE_FP32])
+@pytest.mark.parametrize("mode", [pytest.param(configs.MODE_BF16, marks=MULTI_BLOCK_XFAIL), configs.MODE_FP32])
 def test_config1_two_blocks_gelu_final_norm(mode):
     _case(configs.shrink(W1, n_blocks=2, ffn_kind=configs.FFN_GELU, final_norm=1), mode=mode,
           name=f"cfg1 two blocks gelu final-norm mode{mode}")
@@ -86,45 +87,49 @@ def test_qwen_shapes_reduced_length(wid, N, t):
 # evaluates a subset of KV heads (heads are independent in every sublayer).
 # ----------------------------------------------------------------------------
 
-@pytest.mark.parametrize("wid,layer,heads", [(2, 0, [1, 4]), (2, 18, [2, 6]), (2, 35, [0, 7]), (3, 18, [3]), (4, 0, [5])])
+@pytest.mark.parametrize("wid,layer,heads", [(2, 0, [1, 4]), (2, 18, [2, 6]), (2, 35, [0, 7]), (4, 0, [5])])
 def test_full_size_layer(wid, layer, heads):
     _case(configs.get_workload(wid), layer=layer, heads=heads, name=f"cfg{wid} full layer {layer} heads {heads}")
 
 
-FP32_QWEN_XFAIL = pytest.mark.xfail(
-    reason="fp32 internals reach ~1e-4 here: a pure float32 CPU evaluation of the same layer gives "
-           "1.2e-4/1.5e-4 (C_k/C_v); the cross-attention logit path (X, RMSNorm, Q/K projections) "
-           "would need wider-than-fp32 projections for the refined keys", strict=False)
-
-
-@pytest.mark.parametrize("wid,layer,heads", [pytest.param(2, 1, [2], marks=FP32_QWEN_XFAIL), (4, 3, [1])])
-def test_full_size_fp32_mode(wid, layer, heads):
-    _case(configs.get_workload(wid), layer=layer, heads=heads, mode=configs.MODE_FP32,
-          name=f"cfg{wid} full layer {layer} fp32 mode")
-
-
-def test_config5_first_call_and_teacher_forced_round():
-    """Gemma-shaped iterative compaction: the 64k first call, then one round of
-    [C_k; fresh keys] at positions [out_positions; T..T+8191] recompacted to t."""
-    import numpy as np
-    w = configs.get_workload(5)
-    layer, heads = 41, [6]
+def _both_modes(w, layer, heads, name):
+    """One oracle evaluation, the GPU in bf16 mode (2e-2) and in fp32 validation mode (1e-4)."""
     cache = synth.make_cache(w, layer)
     wts = synth.make_weights(w, layer)
-    log(f"case cfg5 first call layer {layer}")
-    got = run_gpu(w.cfg, cache, wts, w.rope_theta, w.t)
+    log(f"case {name}: oracle heads {heads}")
     ref = run_oracle(w.cfg, cache, wts, w.rope_theta, w.t, heads=heads)
-    assert_parity((got[0][heads], got[1][heads], got[2]), ref, BF16_TOL, what="cfg5 first call")
-    # round 1, teacher-forced on the GPU's bf16 output
-    Ck = synth.bf16_bits(got[0])
-    Cv = synth.bf16_bits(got[1])
-    fresh = synth.make_fresh_tokens(w, layer, 1, start_pos=float(w.n_tokens))
-    rnd = dict(K=np.concatenate([Ck, fresh["K"]], axis=1), V=np.concatenate([Cv, fresh["V"]], axis=1),
-               positions=np.concatenate([got[2], fresh["positions"]]))
-    log(f"case cfg5 round 1 N={rnd['K'].shape[1]}")
-    got1 = run_gpu(w.cfg, rnd, wts, w.rope_theta, w.t)
-    ref1 = run_oracle(w.cfg, rnd, wts, w.rope_theta, w.t, heads=heads)
-    assert_parity((got1[0][heads], got1[1][heads], got1[2]), ref1, BF16_TOL, what="cfg5 round 1")
+    for mode, tol in ((configs.MODE_BF16, BF16_TOL), (configs.MODE_FP32, FP32_TOL)):
+        got = run_gpu(w.cfg, cache, wts, w.rope_theta, w.t, mode=mode)
+        assert_parity((got[0][heads], got[1][heads], got[2]), ref, tol, what=f"{name} mode{mode}")
+    return cache, wts
+
+
+@pytest.mark.parametrize("wid,layer,heads", [(2, 1, [2]), (3, 18, [3]), (4, 3, [1])])
+def test_full_size_both_modes(wid, layer, heads):
+    _both_modes(configs.get_workload(wid), layer, heads, f"cfg{wid} full layer {layer}")
+
+
+def test_config5_iterative_teacher_forced():
+    """Gemma-shaped iterative compaction on one layer: the 64k first call (bf16
+    and fp32 mode against one oracle evaluation), then the 8 rounds of
+    [C_k; fresh keys] at positions [out_positions; T..T+8191] recompacted to t,
+    the GPU chain running free on its own bf16 outputs.  Rounds 1, 4 and 8 are
+    checked teacher-forced: the oracle's round r consumes exactly the input the
+    GPU's round r received (the GPU's round r-1 output)."""
+    w = configs.get_workload(5)
+    layer, heads = 41, [6]
+    cache, wts = _both_modes(w, layer, heads, "cfg5 first call")
+    got = run_gpu(w.cfg, cache, wts, w.rope_theta, w.t)
+    for r in range(1, w.rounds + 1):
+        fresh = synth.make_fresh_tokens(w, layer, r, start_pos=float(w.n_tokens + (r - 1) * w.fresh_tokens))
+        rnd = dict(K=np.concatenate([synth.bf16_bits(got[0]), fresh["K"]], axis=1),
+                   V=np.concatenate([synth.bf16_bits(got[1]), fresh["V"]], axis=1),
+                   positions=np.concatenate([got[2], fresh["positions"]]))
+        log(f"case cfg5 round {r} N={rnd['K'].shape[1]}")
+        got = run_gpu(w.cfg, rnd, wts, w.rope_theta, w.t)
+        if r in (1, 4, 8):
+            ref = run_oracle(w.cfg, rnd, wts, w.rope_theta, w.t, heads=heads)
+            assert_parity((got[0][heads], got[1][heads], got[2]), ref, BF16_TOL, what=f"cfg5 round {r}")
 
 
 # ----------------------------------------------------------------------------
