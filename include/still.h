@@ -229,6 +229,26 @@ still_status still_attend(const still_attend_config *cfg, const void *q, const d
                           const float *beta, const void *K, const void *V, void *out,
                           void *workspace, size_t workspace_bytes, void *stream);
 
+/* still_attend without a caller workspace, for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving (decode) loops,
+ * harnesses that forbid allocation.  The split-N partials live in a
+ * file-scope device array of STILL_ATTEND_SCRATCH_BYTES that every GPU the
+ * library runs on holds until the process ends (its address is looked up once
+ * per device, at the first call made with that device current).  The call
+ * allocates nothing and frees nothing.
+ *
+ * Arguments, layouts, validation and asynchrony as still_attend.
+ * STILL_E_WORKSPACE when still_attend_workspace_size(cfg) exceeds the array
+ * (it never does for n_kv_heads <= 2048); STILL_E_HIP when the device or the
+ * array's address cannot be obtained.  Every call on a GPU shares that GPU's
+ * array: calls that overlap on one GPU (other streams, other threads) race
+ * and must be ordered by the caller; the array keeps the last call's
+ * contents, none of which a later call reads before writing it. */
+enum { STILL_ATTEND_SCRATCH_BYTES = 68 << 20 };
+still_status still_attend_scratch(const still_attend_config *cfg, const void *q, const double *q_positions,
+                                  const void *C_k, const void *C_v, const float *beta, const void *K,
+                                  const void *V, void *out, void *stream);
+
 /* Human-readable name of a status code (static string). */
 const char *still_status_string(int32_t status);
 

@@ -102,6 +102,8 @@ def lib():
         L.still_attend.argtypes = [ctypes.POINTER(still_attend_config), *[ctypes.c_void_p] * 9, ctypes.c_size_t,
                                    ctypes.c_void_p]
         L.still_attend.restype = ctypes.c_int32
+        L.still_attend_scratch.argtypes = [ctypes.POINTER(still_attend_config), *[ctypes.c_void_p] * 9]
+        L.still_attend_scratch.restype = ctypes.c_int32
         L.still_status_string.argtypes = [ctypes.c_int32]
         L.still_status_string.restype = ctypes.c_char_p
         L.still_last_error.argtypes = []
@@ -199,6 +201,16 @@ def still_attend(cfg: still_attend_config, q, q_positions, C_k, C_v, beta, K, V,
     """Raw entry point (pointers or tensors); returns the status code."""
     return lib().still_attend(ctypes.byref(cfg), _ptr(q), _ptr(q_positions), _ptr(C_k), _ptr(C_v), _ptr(beta),
                               _ptr(K), _ptr(V), _ptr(out), _ptr(workspace), workspace_bytes, _ptr(stream))
+
+
+def still_attend_scratch(cfg: still_attend_config, q, q_positions, C_k, C_v, beta, K, V, out, stream) -> int:
+    """Raw entry point of the allocation-free attention (no workspace argument);
+    returns the status code."""
+    return lib().still_attend_scratch(ctypes.byref(cfg), _ptr(q), _ptr(q_positions), _ptr(C_k), _ptr(C_v),
+                                      _ptr(beta), _ptr(K), _ptr(V), _ptr(out), _ptr(stream))
+
+
+STILL_ATTEND_SCRATCH_BYTES = 68 << 20
 
 
 def still_status_string(status: int) -> str:

@@ -6,6 +6,8 @@
 #include "host.hpp"
 #include "refine64.hpp"
 
+#include <mutex>
+
 namespace still {
 
 // per-call tables shared by all layers
@@ -216,6 +218,32 @@ static hipError_t launch_attend(const ConsumerArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Scratch of still_attend_scratch: the split partials of one call, in a
+// file-scope device array (one copy per GPU).  Host code uses the address
+// hipGetSymbolAddress returns for the current device, never the array's name.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[STILL_ATTEND_SCRATCH_BYTES];
+constexpr int SCRATCH_MAX_DEVICES = 64;
+static void* scratch_ptr[SCRATCH_MAX_DEVICES];
+static std::mutex scratch_mu;
+
+static still_status scratch_for_current_device(void** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return fail(STILL_E_UNSUPPORTED, "device %d beyond %d", dev,
+                                                         SCRATCH_MAX_DEVICES);
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(STILL_E_HIP, "hipGetSymbolAddress returned NULL for the scratch array");
+    scratch_ptr[dev] = p;
+  }
+  *out = scratch_ptr[dev];
+  return STILL_OK;
+}
+
 }  // namespace still
 
 using namespace still;
@@ -322,6 +350,20 @@ still_status still_attend(const still_attend_config* cfg, const void* q, const d
   }
   if (e != hipSuccess) return fail(STILL_E_HIP, "attend launch: %s", hipGetErrorString(e));
   return STILL_OK;
+}
+
+still_status still_attend_scratch(const still_attend_config* cfg, const void* q, const double* q_positions,
+                                  const void* C_k, const void* C_v, const float* beta, const void* K, const void* V,
+                                  void* out, void* stream) {
+  AttendPlan ap;
+  still_status s = attend_plan(cfg, &ap);
+  if (s != STILL_OK) return s;
+  if (ap.total > (size_t)STILL_ATTEND_SCRATCH_BYTES)
+    return fail(STILL_E_WORKSPACE, "attend needs %zu bytes of scratch; the static array holds %zu", ap.total,
+                (size_t)STILL_ATTEND_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((s = scratch_for_current_device(&ws)) != STILL_OK) return s;
+  return still_attend(cfg, q, q_positions, C_k, C_v, beta, K, V, out, ws, (size_t)STILL_ATTEND_SCRATCH_BYTES, stream);
 }
 
 const char* still_status_string(int32_t s) {

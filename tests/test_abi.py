@@ -223,3 +223,19 @@ def test_refine_kernel_wk_rows_stay_inside_the_head(dc):
                 rows.update(range(row0, row0 + 32))
     assert min(rows) >= 0 and max(rows) < dc
     assert rows == set(range(dc))   # and every row of the head is used
+
+
+def test_attend_scratch_rejects_oversized_configuration():
+    """A configuration whose split partials exceed the static scratch array is
+    rejected with STILL_E_WORKSPACE before anything is enqueued (no device
+    access: every pointer is fake)."""
+    acfg = binding.still_attend_config(4096, 8, 256, 4, 64, 64, 0, 0.0, configs.MODE_BF16, 0.0)
+    assert binding.still_attend_workspace_size(acfg) > binding.STILL_ATTEND_SCRATCH_BYTES
+    st = binding.still_attend_scratch(acfg, FAKE, None, FAKE, FAKE, None, FAKE, FAKE, FAKE, None)
+    assert st == -4
+    assert "scratch" in binding.still_last_error()
+
+
+def test_attend_scratch_size_matches_header():
+    m = re.search(r"STILL_ATTEND_SCRATCH_BYTES\s*=\s*(\d+)\s*<<\s*(\d+)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == binding.STILL_ATTEND_SCRATCH_BYTES
