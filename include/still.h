@@ -229,6 +229,39 @@ still_status still_attend(const still_attend_config *cfg, const void *q, const d
                           const float *beta, const void *K, const void *V, void *out,
                           void *workspace, size_t workspace_bytes, void *stream);
 
+/* -------------------------------------------------------------------------
+ * Backward pass of one layer's compactor (the training hot path without the
+ * base model and its loss; Section 2.4 and Appendix E).  With upstream
+ * gradients dC_k, dC_v of the layer's outputs, writes the gradient of
+ *     L = <dC_k, C_k> + <dC_v, C_v>
+ * with respect to every compactor tensor (the cache K, V gets none).
+ *
+ *   cfg            as for the forward pass; mode must be STILL_MODE_FP32
+ *                  (all buffers float32), at most 8 blocks
+ *   w, K, V, positions, N, rope_theta, t, flags   as still_compact_layer
+ *   dC_k, dC_v     [H][t][d] float32 device buffers
+ *   grad           a still_layer_weights of gradient OUTPUT buffers, one per
+ *                  tensor of w with the same shape (float32, device):
+ *                  grad->latents [H][t][D] (t_bank must equal t), the host
+ *                  array grad->blocks[n_blocks], grad->w_key, grad->w_val.
+ *                  A NULL entry skips that gradient.  Every non-NULL buffer
+ *                  is overwritten (not accumulated into).
+ *   C_k, C_v       optional [H][t][d] float32 outputs of the same forward
+ *                  pass (NULL = not written)
+ *   workspace      >= still_backward_workspace_size(cfg, N, t) bytes: the
+ *                  forward intermediates kept for the chain rule, including
+ *                  every attention probability (H n_c t N floats per
+ *                  cross-attention block)
+ * STILL_E_UNSUPPORTED in bf16 mode; other errors and asynchrony as the
+ * compaction calls.
+ * ------------------------------------------------------------------------- */
+size_t still_backward_workspace_size(const still_config *cfg, int64_t N, int32_t t);
+still_status still_compact_layer_backward(const still_config *cfg, const still_layer_weights *w, const void *K,
+                                          const void *V, const double *positions, int64_t N, double rope_theta,
+                                          int32_t t, uint32_t flags, const void *dC_k, const void *dC_v,
+                                          const still_layer_weights *grad, void *C_k, void *C_v, void *workspace,
+                                          size_t workspace_bytes, void *stream);
+
 /* still_attend without a caller workspace, for callers that cannot allocate
  * device memory: code under HIP graph capture, tight serving (decode) loops,
  * harnesses that forbid allocation.  The split-N partials live in a

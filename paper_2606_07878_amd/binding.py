@@ -102,6 +102,15 @@ def lib():
         L.still_attend.argtypes = [ctypes.POINTER(still_attend_config), *[ctypes.c_void_p] * 9, ctypes.c_size_t,
                                    ctypes.c_void_p]
         L.still_attend.restype = ctypes.c_int32
+        L.still_backward_workspace_size.argtypes = [ctypes.POINTER(still_config), ctypes.c_int64, ctypes.c_int32]
+        L.still_backward_workspace_size.restype = ctypes.c_size_t
+        L.still_compact_layer_backward.argtypes = [ctypes.POINTER(still_config),
+                                                   ctypes.POINTER(still_layer_weights), ctypes.c_void_p,
+                                                   ctypes.c_void_p, *common, ctypes.c_void_p, ctypes.c_void_p,
+                                                   ctypes.POINTER(still_layer_weights), ctypes.c_void_p,
+                                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                                   ctypes.c_void_p]
+        L.still_compact_layer_backward.restype = ctypes.c_int32
         L.still_attend_scratch.argtypes = [ctypes.POINTER(still_attend_config), *[ctypes.c_void_p] * 9]
         L.still_attend_scratch.restype = ctypes.c_int32
         L.still_status_string.argtypes = [ctypes.c_int32]
@@ -306,6 +315,46 @@ def compact_layer(cfg: configs.CompactorConfig, weights: Dict[str, object], K, V
                                STILL_F_REROTATE if rerotate else 0, Ck, Cv, outp, workspace,
                                workspace.numel(), stream))
     return Ck, Cv, outp
+
+
+def still_backward_workspace_size(cfg: still_config, N: int, t: int) -> int:
+    return int(lib().still_backward_workspace_size(ctypes.byref(cfg), N, t))
+
+
+def still_compact_layer_backward(cfg: still_config, w: LayerWeights, K, V, positions, N: int, rope_theta: float,
+                                 t: int, flags: int, dC_k, dC_v, grad: LayerWeights, C_k, C_v, workspace,
+                                 workspace_bytes: int, stream) -> int:
+    """Raw entry point (pointers or tensors); returns the status code."""
+    return lib().still_compact_layer_backward(ctypes.byref(cfg), ctypes.byref(w.struct), _ptr(K), _ptr(V),
+                                              _ptr(positions), N, rope_theta, t, flags, _ptr(dC_k), _ptr(dC_v),
+                                              ctypes.byref(grad.struct), _ptr(C_k), _ptr(C_v), _ptr(workspace),
+                                              workspace_bytes, _ptr(stream))
+
+
+def compact_layer_backward(cfg: configs.CompactorConfig, weights: Dict[str, object], K, V, positions,
+                           rope_theta: float, t: int, dC_k, dC_v, rerotate: bool = True, workspace=None):
+    """Gradients of <dC_k, C_k> + <dC_v, C_v> w.r.t. every compactor tensor
+    (fp32 mode) through still_compact_layer_backward; returns (grads dict
+    keyed like ``weights``, C_k, C_v) as float32 tensors on K's device."""
+    torch = _torch()
+    dev = K.device
+    ccfg = make_config(cfg, configs.MODE_FP32)
+    N = int(K.shape[1])
+    need = still_backward_workspace_size(ccfg, N, t)
+    if need == 0:
+        raise StillError(-5, "configuration rejected by still_backward_workspace_size")
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    grads = {k: torch.empty(tuple(v.shape), dtype=torch.float32, device=dev) for k, v in weights.items()}
+    Ck = torch.empty(cfg.n_kv_heads, t, cfg.head_dim, dtype=torch.float32, device=dev)
+    Cv = torch.empty_like(Ck)
+    lw = weights if isinstance(weights, LayerWeights) else LayerWeights(cfg, weights)
+    gw = LayerWeights(cfg, grads)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(still_compact_layer_backward(ccfg, lw, K, V, positions, N, rope_theta, t,
+                                        STILL_F_REROTATE if rerotate else 0, dC_k, dC_v, gw, Ck, Cv, workspace,
+                                        workspace.numel(), stream))
+    return grads, Ck, Cv
 
 
 def compact_subrange(cfg: configs.CompactorConfig, weights: Dict[str, object], K, V, positions, rope_theta: float,

@@ -1,8 +1,9 @@
 """Build libstill.so (HIP, gfx950) in-tree with hipcc.
 
-The library is three translation units compiled in parallel (the C ABI and
+The library is four translation units compiled in parallel (the C ABI and
 the consumer attention; the per-layer launch sequence for bf16 I/O; the same
-for the fp32 validation mode) and linked into one shared object."""
+for the fp32 validation mode; the backward pass) and linked into one shared
+object."""
 from __future__ import annotations
 
 import os
@@ -13,10 +14,10 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libstill.so")
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = [os.path.join(CSRC, f) for f in ("still.hip", "layer_bf16.hip", "layer_fp32.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("still.hip", "layer_bf16.hip", "layer_fp32.hip", "backward.hip")]
 HEADERS = [os.path.join(CSRC, f) for f in ("common.hpp", "gemm.hpp", "attn.hpp", "misc.hpp", "kproj.hpp",
                                            "consumer.hpp", "refine.hpp", "refine64.hpp", "host.hpp",
-                                           "layer.hpp")] + [os.path.join(ROOT, "include", "still.h")]
+                                           "layer.hpp", "bwd.hpp")] + [os.path.join(ROOT, "include", "still.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

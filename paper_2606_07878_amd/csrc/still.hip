@@ -38,54 +38,6 @@ static still_status prepare_tables(const Dims& m, const Plan& p, char* ws, const
   return STILL_OK;
 }
 
-// ---------------------------------------------------------------------------
-// Validation of a layer's pointers
-// ---------------------------------------------------------------------------
-static bool misaligned(const void* p) { return ((uintptr_t)p & 15u) != 0; }
-
-static still_status check_ptr(const void* p, const char* name, bool required) {
-  if (!p) return required ? fail(STILL_E_INVAL, "%s is NULL", name) : STILL_OK;
-  if (misaligned(p)) return fail(STILL_E_INVAL, "%s is not 16-byte aligned", name);
-  return STILL_OK;
-}
-
-static still_status check_layer(const still_config* c, const Dims& m, const still_layer_weights* w, int layer) {
-  if (!w) return fail(STILL_E_INVAL, "layer %d: weights NULL", layer);
-  if (w->t_bank != m.t) return fail(STILL_E_SHAPE, "layer %d: t=%d but latent bank holds %d", layer, m.t, w->t_bank);
-  still_status s;
-#define CHK(p, req)                                                        \
-  if ((s = check_ptr((p), #p, (req))) != STILL_OK) {                       \
-    g_last_error = "layer " + std::to_string(layer) + ": " + g_last_error; \
-    return s;                                                              \
-  }
-  CHK(w->latents, true);
-  CHK(w->w_key, true);
-  CHK(w->w_val, true);
-  if (!w->blocks) return fail(STILL_E_INVAL, "layer %d: blocks NULL", layer);
-  for (int b = 0; b < c->n_blocks; ++b) {
-    const still_block_weights& bw = w->blocks[b];
-    const bool ca = c->cross_every_block || b == 0;
-    CHK(bw.ca_wq, ca);
-    CHK(bw.ca_bq, false);
-    CHK(bw.ca_wk, ca);
-    CHK(bw.ca_bk, false);
-    CHK(bw.ca_wv, ca);
-    CHK(bw.ca_wo, ca);
-    const bool sa = m.ns > 0;
-    CHK(bw.sa_wq, sa);
-    CHK(bw.sa_bq, false);
-    CHK(bw.sa_wk, sa);
-    CHK(bw.sa_bk, false);
-    CHK(bw.sa_wv, sa);
-    CHK(bw.sa_wo, sa);
-    CHK(bw.ffn_wg, c->ffn_kind == STILL_FFN_SWIGLU);
-    CHK(bw.ffn_wu, c->ffn_kind != STILL_FFN_NONE);
-    CHK(bw.ffn_wd, c->ffn_kind != STILL_FFN_NONE);
-  }
-#undef CHK
-  return STILL_OK;
-}
-
 static still_status compact(const still_config* cfg, int32_t L, const still_layer_weights* w, const void* const* K,
                             const void* const* V, const double* positions, int64_t N, double rope_theta, int32_t t,
                             uint32_t flags, void* const* Ck, void* const* Cv, double* out_positions,

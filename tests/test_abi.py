@@ -239,3 +239,16 @@ def test_attend_scratch_rejects_oversized_configuration():
 def test_attend_scratch_size_matches_header():
     m = re.search(r"STILL_ATTEND_SCRATCH_BYTES\s*=\s*(\d+)\s*<<\s*(\d+)", open(HEADER).read())
     assert m and int(m.group(1)) << int(m.group(2)) == binding.STILL_ATTEND_SCRATCH_BYTES
+
+
+def test_backward_rejects_bf16_mode_and_sizes_fp32_only():
+    c16 = _cfg()
+    assert binding.still_backward_workspace_size(c16, 2048, 256) == 0
+    c32 = _cfg(mode=1)
+    assert binding.still_backward_workspace_size(c32, 2048, 256) > 0
+    w = FakeWeights(c16, 256)
+    g = FakeWeights(c16, 256)
+    st = binding.lib().still_compact_layer_backward(ctypes.byref(c16), ctypes.byref(w.struct), FAKE, FAKE, FAKE, 2048,
+                                                    1e6, 256, 1, FAKE, FAKE, ctypes.byref(g.struct), None, None,
+                                                    FAKE, 1 << 40, None)
+    assert st == -5 and "FP32" in binding.still_last_error()
