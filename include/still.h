@@ -38,6 +38,12 @@
  *   execution surface at the caller's next synchronisation.
  * - Outputs must not alias inputs or the workspace.  NaN/Inf in the inputs
  *   are not checked and propagate.
+ * - Magnitudes, STILL_MODE_BF16: the MFMA operands are fp16 (max 65504).  The
+ *   cache K, V may hold any finite bf16 value: each KV head is staged scaled
+ *   by an exact power of two that brings its max |K|, |V| within 2^14 (1 for
+ *   ordinary caches), undone on the value path.  Weights, biases and latents
+ *   are converted to fp16 as they are and must lie within +-65504 (larger
+ *   values overflow to +-inf and make the outputs non-finite).
  * - Calls that share a workspace must be ordered on one stream.
  */
 #ifndef STILL_H_

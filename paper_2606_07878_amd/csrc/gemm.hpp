@@ -73,6 +73,10 @@ struct GemmArgs {
   long ldqex, sE1, sE2;
   float2* rpart;
   long sR1, sR2;
+  // RESID: optional per-row factor of the product, rowscale[row / rowscale_div]
+  // (undoes the fp16 range scale of the value path per KV head)
+  const float* rowscale;
+  int rowscale_div;
   float scale;         // SCALE: C = acc * scale * rq[r] * rk[col]
   const float* rq;
   long ldrq, sQ1, sQ2;
@@ -401,6 +405,16 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
           stg[rl * SLD + b * 32 + l32] = acc[a][b][j] * sc_f[lbase + rl] * sc_f[BM + col_base(b) + l32];
       }
     } else if constexpr (!PAIRED) {
+      float rsc[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) rsc[j] = 1.f;
+      if (EPI == EPI_RESID && g.rowscale) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const long r = grow(lbase + 8 * (j >> 2) + 4 * lg + (j & 3));
+          rsc[j] = r >= 0 ? g.rowscale[r / g.rowscale_div] : 0.f;
+        }
+      }
 #pragma unroll
       for (int b = 0; b < TN; ++b) {
         const int col = nt * BN + col_base(b) + l32;
@@ -408,7 +422,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
-          float v = acc[a][b][j];
+          float v = acc[a][b][j] * rsc[j];
           if constexpr (EPI == EPI_GELU) {
             v = gelu_f(v + bv);
           } else if constexpr (EPI != EPI_RESID) {

@@ -146,6 +146,7 @@ struct Plan {
   size_t X, XT, Z, Y, q, partq, rq, O;
   size_t Ylo, qex, cval, cidx, ocnt, ridx, rval, rcnt, rpart, crow, ccount;   // logit refinement
   size_t q64, invf_b, invf_c;   // fp32 mode: fp64 queries and RoPE frequencies of the refinement
+  size_t kvpart, hscale;        // bf16 mode: per-head fp16 range scale of the staged cache
   // union region: cross-attention key side ...
   size_t k, partk, rk, opart, mpart, lpart;
   // ... or self-attention / FFN buffers
@@ -265,6 +266,15 @@ inline long matrix_elems(const still_config* c, const Dims& m) {
   return total;
 }
 
+// Cache rows per workgroup of the RoPE-fix staging kernel (its LDS tile of
+// rows x (2d + 8) elements stays within 40 KB) and its workgroups per head.
+inline int stage_rows(const Dims& m) {
+  int RW = 64;
+  while (RW > 8 && (size_t)RW * (m.d2 + 8) * m.cs > 40960) RW /= 2;
+  return RW;
+}
+inline int stage_blocks(const Dims& m) { return (int)((m.Npad + stage_rows(m) - 1) / stage_rows(m)); }
+
 inline Plan make_plan(const still_config* c, const Dims& m) {
   Plan p;
   size_t off = 0;
@@ -282,6 +292,8 @@ inline Plan make_plan(const still_config* c, const Dims& m) {
   p.tab_bk = take(8ul * m.N * (m.d / 2));
   p.tab_bq = take(8ul * m.t * (m.d / 2));
   p.wconv = m.fp32 ? 0 : take(2ul * matrix_elems(c, m));
+  p.kvpart = m.fp32 ? 0 : take(4ul * m.H * stage_blocks(m));
+  p.hscale = m.fp32 ? 0 : take(4ul * 2 * m.H);
   p.wkt = m.fp32 ? 0 : take(2ul * m.Ec * m.d2);
   p.X = take(cs * HN * m.d2);
   p.XT = take(cs * (size_t)m.H * m.d2 * m.Npad);

@@ -56,6 +56,7 @@ struct KprojArgs {
   const float2* tab;    // [N][dc/2] (cos, sin) of the compactor RoPE at the key positions
   f16* k;               // tiled keys (ktile_off with npad keys per head), permuted widths
   float* part;          // [nc][H*N] sum of squares of k~ (one partial per row and cross head)
+  const float* hscale;  // [H] fp16 range scale of the staged X of each KV head (the bias is scaled with it), or NULL
   int H, N, nc, dc, kpw;
   long npad;
 };
@@ -101,12 +102,14 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
   // this lane's key in each key tile: row, KV head, key index
   int kh[4], kn[4];
   bool kok[4];
+  float bsc[4];   // bias scale of the key's KV head
 #pragma unroll
   for (int kt = 0; kt < 4; ++kt) {
     const int r = 32 * kt + l32;
     kh[kt] = r / kpw;
     kn[kt] = n0 + (r - kh[kt] * kpw);
     kok[kt] = kh[kt] < a.H && kn[kt] < a.N;
+    bsc[kt] = (a.hscale && kh[kt] < a.H) ? a.hscale[kh[kt]] : 1.f;
   }
   // Every wave runs the same loop trip counts (the barriers are workgroup
   // wide); wave w computes cross heads w + 4 (cb + i) that exist.
@@ -200,7 +203,7 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
               const int j = 4 * q + u;
-              const float blo = bias_at(bl[q], u), bhi = bias_at(bu[q], u);
+              const float blo = bias_at(bl[q], u) * bsc[kt], bhi = bias_at(bu[q], u) * bsc[kt];
               const float ylo = acc[0][kt][j] + blo, yhi = acc[1][kt][j] + bhi;
               ss += ylo * ylo + yhi * yhi;
               olo[j >> 3][j & 7] = (f16)(ylo * cs[u] - yhi * sn[u]);

@@ -151,16 +151,26 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
     w = &cw;
   }
 
-  // RoPE-fix staging of X = [R(-p) K ; V] and X^T
+  // RoPE-fix staging of X = [R(-p) K ; V] and X^T.  fp16 operands: the first
+  // pass also finds each head's max |K|, |V|; heads beyond the fp16 range
+  // (scale != 1) are staged again, scaled by an exact power of two.
   {
-    int RW = 64;
-    while (RW > 8 && (size_t)RW * (m.d2 + 8) * m.cs > 40960) RW /= 2;
+    const int RW = stage_rows(m);
     const size_t lds = (size_t)RW * (m.d2 + 8) * m.cs;
-    dim3 grid((unsigned)((m.Npad + RW - 1) / RW), m.H);
+    const dim3 grid((unsigned)stage_blocks(m), m.H);
     TIMED(STILL_K_STAGE);
+    float* part = sizeof(CT) == 2 ? (float*)(ws + p.kvpart) : nullptr;
+    float* hscale = sizeof(CT) == 2 ? (float*)(ws + p.hscale) : nullptr;
     hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, tab_bk, m.N,
-                       m.d, X, XT, m.Npad, RW);
+                       m.d, X, XT, m.Npad, RW, part, (const float*)hscale, 0);
     HIP_TRY(hipGetLastError());
+    if (hscale) {
+      hipLaunchKernelGGL(kv_scale_kernel, dim3(m.H), dim3(256), 0, st, (const float*)part, (int)grid.x, m.H, hscale);
+      HIP_TRY(hipGetLastError());
+      hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, tab_bk,
+                         m.N, m.d, X, XT, m.Npad, RW, (float*)nullptr, (const float*)hscale, 1);
+      HIP_TRY(hipGetLastError());
+    }
   }
   {
     TIMED(STILL_K_OTHER);
@@ -232,6 +242,7 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
         ka.nc = m.nc;
         ka.dc = m.dc;
         ka.npad = m.Npad;
+        ka.hscale = (const float*)(ws + p.hscale);
         // table stage capacity 16, 64 or 128 key positions (LDS <= 160 KB)
         ka.kpw = 128 / m.H;
         const dim3 grid((unsigned)((m.N + ka.kpw - 1) / ka.kpw));
@@ -333,6 +344,7 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
               rk_.count = ccount;
               rk_.qex = (const float*)(ws + p.qex);
               rk_.rpart = (float2*)(ws + p.rpart);
+              rk_.hscale = (const float*)(ws + p.hscale);
               rk_.N = m.N;
               rk_.t = m.t;
               rk_.R = m.R;
@@ -429,8 +441,12 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
         g.sC2 = m.dc;
         HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE, true>(g, m.nc, st)));
       }
-      {  // Z += Concat(heads) W_O^T
+      {  // Z += Concat(heads) W_O^T (times 2^e_h: the value path carried the fp16 range scale)
         GemmArgs g = gargs((int)Ht, m.D, m.Ec, head, m.Ec, bw.ca_wo, m.Ec, Z, m.D);
+        if (!m.fp32) {
+          g.rowscale = (const float*)(ws + p.hscale) + m.H;   // 2^e_h
+          g.rowscale_div = m.t;
+        }
         HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID, true>(g, 1, st)));
       }
     }

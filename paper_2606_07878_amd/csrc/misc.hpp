@@ -97,14 +97,56 @@ template <class T> __device__ __forceinline__ void store8(T* p, const float (&v)
   }
 }
 
+// ---------------------------------------------------------------------------
+// fp16 range of the staged cache.  The fp16 operands hold magnitudes up to
+// 65504 while bf16 inputs reach 3.4e38, so each KV head's X = [R(-p) K; V]
+// is staged times a power of two 2^-e_h, e_h >= 0 the smallest exponent that
+// brings max(|K|, |V|) of the head to at most 2^14 (the rotation keeps the
+// norm of each pair).  The scaling is exact, leaves the keys' directions
+// (hence the QK-normed logits) unchanged when the key bias is scaled with
+// them, and is undone on the value path by the output projection; for caches
+// within 2^14 it is 1 and changes nothing.
+// ---------------------------------------------------------------------------
+// scale[h] = 2^-e_h and scale[H + h] = 2^e_h from the per-workgroup maxima
+// of |K|, |V| that the staging pass wrote for head h.  One workgroup per head.
+static __global__ __launch_bounds__(256) void kv_scale_kernel(const float* __restrict__ part, int nblk, int H,
+                                                       float* __restrict__ scale) {
+  __shared__ float red[4];
+  const int h = blockIdx.x;
+  float m = 0.f;
+  for (int b = threadIdx.x; b < nblk; b += 256) m = fmaxf(m, part[(long)h * nblk + b]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    float s = 1.f, inv = 1.f;
+    while (m * s > 16384.f) {   // at most ~113 halvings (m < 2^128; NaN stops at once)
+      s *= 0.5f;
+      inv *= 2.f;
+    }
+    scale[h] = s;
+    scale[H + h] = inv;
+  }
+}
+
+// Staging passes: pass 0 stages every head unscaled and, with `part`,
+// writes each workgroup's max(|K|, |V|) (part[h][blockIdx.x]); pass 1
+// re-stages, times hscale[h], only the heads whose scale is not 1 (the
+// workgroups of the other heads exit at once).
 template <class IT, class CT>
 __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, const IT* __restrict__ V,
                                                       const float2* __restrict__ tab, long N, int d,
                                                       CT* __restrict__ X, CT* __restrict__ XT, long ldxt,
-                                                      int RW) {
+                                                      int RW, float* __restrict__ part, const float* __restrict__ hscale,
+                                                      int pass) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem_raw[];
   CT* tile = (CT*)smem_raw;              // [RW][2d + 8]
   const int h = blockIdx.y;
+  const float sc = pass ? hscale[h] : 1.f;   // fp16 range scale of this head (exact power of two)
+  if (sc == 1.f && pass) return;             // uniform
+  float amax = 0.f;
   const long n0 = (long)blockIdx.x * RW;
   const int d2 = 2 * d, hh = d / 2, ld = d2 + 8;
   const IT* Kh = K + (long)h * N * d;
@@ -122,6 +164,8 @@ __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, 
         float a[8], b[8];
         load8(Kh + n * d + j, a);
         load8(Kh + n * d + j + hh, b);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) amax = fmaxf(amax, fmaxf(fabsf(a[u]), fabsf(b[u])));
         const f32x4* tp = (const f32x4*)(tab + n * hh + j);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -131,6 +175,11 @@ __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, 
           y1[2 * u] = b[2 * u] * cs[0] - a[2 * u] * cs[1];
           y0[2 * u + 1] = a[2 * u + 1] * cs[2] + b[2 * u + 1] * cs[3];
           y1[2 * u + 1] = b[2 * u + 1] * cs[2] - a[2 * u + 1] * cs[3];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          y0[u] *= sc;
+          y1[u] *= sc;
         }
         store8(xr + j, y0);
         store8(xr + j + hh, y1);
@@ -145,6 +194,11 @@ __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, 
       float v[8];
       if (n < N) {
         load8(Vh + n * d + f, v);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          amax = fmaxf(amax, fabsf(v[u]));
+          v[u] *= sc;
+        }
         store8(xr + d + f, v);
       } else {
 #pragma unroll
@@ -152,6 +206,14 @@ __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, 
       }
       store8(tile + r * ld + d + f, v);
     }
+  }
+  if (part) {   // this workgroup's max |K|, |V| (reduced through the LDS tile's tail before phase 2 reuses nothing)
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o));
+    __shared__ float red[4];
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = amax;
+    __syncthreads();
+    if (threadIdx.x == 0) part[(long)h * gridDim.x + blockIdx.x] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   }
   __syncthreads();
   // phase 2: X^T, 8 keys per store: the fragment-tiled layout of the fp16

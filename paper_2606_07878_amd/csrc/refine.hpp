@@ -38,6 +38,7 @@ struct RefineKArgs {
   const int* count;       // [H*nc] rows in each list
   const float* qex;       // [H][t][nc*dc] fp32 q~
   float2* rpart;          // [H*nc][t*R] (dot, sum of squares) per slot
+  const float* hscale;    // [H] fp16 range scale of each KV head's rows (applied to the rows and b_K), or NULL
   long N;
   int t, R, H, nc, dc;
   int ntile;              // row tiles per list the grid covers (ntile * H * nc workgroups, looping)
@@ -87,6 +88,7 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
   const int cnt = a.count[b];                     // uniform
   const int TR = a.t * a.R;
   const int hh = a.dc >> 1;
+  const float hsc = a.hscale ? a.hscale[h] : 1.f;
   const long Ec = (long)a.nc * a.dc;
   const int* crow = a.crow + (long)b * TR;
   const int* ridx = a.ridx + (long)b * TR;
@@ -133,15 +135,16 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
       half4 h0, h1, l0, l1, w0, w1;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        // un-rotation of the base RoPE (rotate-half pairs j, j + d/2)
-        const float y0 = k0[u] * cc[u] + k1[u] * ss[u];
-        const float y1 = k1[u] * cc[u] - k0[u] * ss[u];
+        // un-rotation of the base RoPE (rotate-half pairs j, j + d/2), then
+        // the head's fp16 range scale
+        const float y0 = (k0[u] * cc[u] + k1[u] * ss[u]) * hsc;
+        const float y1 = (k1[u] * cc[u] - k0[u] * ss[u]) * hsc;
         h0[u] = (f16)y0;
         h1[u] = (f16)y1;
         l0[u] = (f16)(y0 - (float)h0[u]);
         l1[u] = (f16)(y1 - (float)h1[u]);
-        w0[u] = (f16)v0[u];
-        w1[u] = (f16)v1[u];
+        w0[u] = (f16)(v0[u] * hsc);
+        w1[u] = (f16)(v1[u] * hsc);
       }
       *(half4*)&row[j] = h0;
       *(half4*)&row[j + HD] = h1;
@@ -221,8 +224,8 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
           }
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            bs0[4 * jq + u] = t0[u];
-            bs1[4 * jq + u] = t1[u];
+            bs0[4 * jq + u] = t0[u] * hsc;
+            bs1[4 * jq + u] = t1[u] * hsc;
           }
         }
 #pragma unroll

@@ -206,3 +206,32 @@ def test_identity_init_reproduces_cache(theta):
         ek, ev = slice_errors(got[0], K).max(), slice_errors(got[1], V).max()
         log(f"identity init theta={theta:g} mode{mode}: |C_k - K| {ek:.3e}  |C_v - V| {ev:.3e}")
         assert ek <= tol and ev <= tol
+
+
+# ----------------------------------------------------------------------------
+# Cache magnitudes beyond the fp16 operands' range (bf16 I/O allows 3.4e38)
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("wid,outlier,vscale,N,t", [(1, 1e5, 1.0, 2048, 256), (1, 10.0, 1e5, 2048, 256),
+                                                     (2, 1e4, 1.0, 2240, 256)])
+def test_large_cache_magnitudes(wid, outlier, vscale, N, t):
+    """Keys with 4 outlier channels per head of standard deviation 1e5
+    (cfg 1, max ~5e5) or 1e4 (Qwen shape, max ~5e4), or values of standard
+    deviation 1e5: bf16 represents them, fp16 (max 65504) does not, or only
+    with no headroom.  The bf16 path stages each KV head scaled by a power of
+    two and must match the oracle like any other cache."""
+    import dataclasses
+    w = dataclasses.replace(configs.get_workload(wid), outlier_channels=4, outlier_scale=outlier)
+    cache = synth.make_cache(w, 0, n_tokens=N)
+    if vscale != 1.0:
+        cache["V"] = synth.bf16_bits(synth.bf16_value(cache["V"]) * vscale)
+    kmax, vmax = np.abs(synth.bf16_value(cache["K"])).max(), np.abs(synth.bf16_value(cache["V"])).max()
+    log(f"case large magnitudes: cfg{wid} max|K| {kmax:.3g} max|V| {vmax:.3g}")
+    assert max(kmax, vmax) > 16384
+    wts = synth.make_weights(w, 0, t=t)
+    heads = [0, 1] if wid == 1 else [0, 5]
+    ref = run_oracle(w.cfg, cache, wts, w.rope_theta, t, heads=heads)
+    for mode, tol in MODES:
+        got = run_gpu(w.cfg, cache, wts, w.rope_theta, t, mode=mode)
+        assert_parity((got[0][heads], got[1][heads], got[2]), ref, tol,
+                      what=f"large magnitudes cfg{wid} K x{outlier:g} V x{vscale:g} mode{mode}")
