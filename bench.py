@@ -353,6 +353,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (HBM counter calibration)")
+    ap.add_argument("--no-consumer", action="store_true",
+                    help="skip the decode-attention measurement (shorter profiler runs)")
     ap.add_argument("--consumer-only", action="store_true",
                     help="time only the decode attention over the compacted and the full cache (after one "
                          "compaction step) and print that object")
@@ -374,7 +376,7 @@ def main():
         res = run_workload(args.workload, 1, args.warmup, dev, binding, consumer=True)
         print(json.dumps({"consumer_attend": res["consumer_attend"], "config": {"workload": w.name}}), flush=True)
         return
-    head = run_workload(args.workload, args.steps, args.warmup, dev, binding, consumer=True)
+    head = run_workload(args.workload, args.steps, args.warmup, dev, binding, consumer=not args.no_consumer)
     extras = [int(x) for x in args.extra_workloads.split(",") if x.strip() and int(x) != args.workload]
     workloads = {}
     for wid in extras:

@@ -69,7 +69,11 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
   constexpr int RING = 2;             // W_K fragment prefetch depth (k steps)
   static_assert(KS % RING == 0, "k steps");
   __shared__ __attribute__((aligned(16))) f16 Xs[128 * LX];
-  __shared__ __attribute__((aligned(16))) float2 Ts[2 * TPW * 32];
+  // table stage rows of 32 (cos, sin) pairs, padded to 34 so that the lanes
+  // of a wave reading the same pairs of different key positions hit
+  // different LDS banks (a 256-byte stride maps every row to one bank group)
+  constexpr int TS = 34;
+  __shared__ __attribute__((aligned(16))) float2 Ts[2 * TPW * TS];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -94,7 +98,7 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
       const int n = n0 + pos;
       f32x4 cs = {1.f, 0.f, 1.f, 0.f};
       if (n < a.N) cs = *(const f32x4*)(a.tab + (long)n * hh + 32 * p + j2);
-      *(f32x4*)&Ts[(buf * kpw + pos) * 32 + j2] = cs;
+      *(f32x4*)&Ts[(buf * kpw + pos) * TS + j2] = cs;
     }
   };
   load_tab(0, 0);
@@ -133,7 +137,7 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
       __syncthreads();                       // X rows / table tile p visible; the other buffer free
       if (p + 1 < NPT) load_tab(p + 1, tb ^ 1);
       else if (cb + 2 < rounds) load_tab(0, tb ^ 1);   // the next pair of cross heads restarts at tile 0
-      const float2* T = Ts + (size_t)tb * kpw * 32;
+      const float2* T = Ts + (size_t)tb * kpw * TS;
 #pragma unroll 1
       for (int i = 0; i < 2; ++i) {
         const int c = w + 4 * (cb + i);
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) {
           const int pos = kn[kt] - n0;
-          const float2* tr = T + (kok[kt] ? pos : 0) * 32;
+          const float2* tr = T + (kok[kt] ? pos : 0) * TS;
           half8 olo[2], ohi[2];
           float ss = 0.f;
 #pragma unroll
