@@ -30,6 +30,9 @@ struct AttnArgs {
   const void* xt;    // X^T (CT), zero beyond N: fp32 kernel [H][2d][ldxt], fp16 kernel tiled (xtile_off)
   long ldxt;
   long npad;         // fp16 kernel: keys per head in the tiled layouts (a multiple of 256)
+  long xfeat, xcoff; // fp16 kernel: features per KV head in the tiled values and the first
+                     //   feature of head c at c * xcoff (cross-attention: 2d and 0, every head
+                     //   reads all of X; self-attention: n_s * d_s and d_s, one value slice per head)
   float* opart;      // [S][H*nc][t][2d]
   float* mpart;      // [S][H*nc][t]
   float* lpart;      // [S][H*nc][t]
@@ -350,7 +353,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
   const f16* qb = (const f16*)a.q + (long)h * a.t * a.ldq + (long)c * a.dc;
   const f16* kb = (const f16*)a.k + (long)hc * a.npad * a.dc;
-  const f16* xtb = (const f16*)a.xt + (long)h * a.d2 * a.npad;
+  const f16* xtb = (const f16*)a.xt + ((long)h * a.xfeat + (long)c * a.xcoff) * a.npad;
   const float* rkb = a.rk + (long)h * a.N * a.nc + c;
   const unsigned ksteps = (unsigned)(a.dc >> 4);   // width steps of one key tile
   const unsigned nsteps = (unsigned)(a.npad >> 4); // key steps of one feature tile

@@ -20,19 +20,20 @@
 //           fp32 copy of the result).
 //   SWIGLU: pair P -> row P of W_g (half 0) and of W_u (half 1);
 //           out[:, P] = SiLU(g) * u.
-//   REFINE: PAIR rotation of gathered key rows, dotted with a query row
-//           (partial dot products and sums of squares instead of a store).
 // Other epilogues: STORE (+bias), GELU (+bias), RESID (C += acc, fp32),
 // SCALE (acc * scale * rq[row] * rk[col]).
 #pragma once
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace still {
 
-enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_PAIR = 2, EPI_SWIGLU = 3, EPI_SCALE = 4, EPI_GELU = 5, EPI_REFINE = 6 };
+enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_PAIR = 2, EPI_SWIGLU = 3, EPI_SCALE = 4, EPI_GELU = 5 };
+enum CTileKind { CTILE_NONE = 0, CTILE_KEYS = 1, CTILE_VALUES = 2 };
 
 struct GemmArgs {
-  int M, N, K;   // N = output columns, or column pairs for PAIR / SWIGLU / REFINE
+  int M, N, K;   // N = output columns, or column pairs for PAIR / SWIGLU
   int nb2;       // batch index z -> (z / nb2, z % nb2), strides s*1, s*2 (elements)
   const void* A;
   const void* A2;      // optional low part of a split A operand: C = (A + A2) B^T, same layout as A
@@ -51,8 +52,8 @@ struct GemmArgs {
   long ldc, sC1, sC2;
   const void* bias;    // per output column, NULL = none
   long sBias2;         // bias offset per unit of the inner batch index
-  int hd;              // PAIR / REFINE: head width
-  const float2* tab;   // rotation table, row (r % tab_mod) (REFINE: row ridx[r]), entry [row*hd/2 + j]; NULL = none
+  int hd;              // PAIR: head width
+  const float2* tab;   // rotation table, row (r % tab_mod), entry [row*hd/2 + j]; NULL = none
   int tab_mod;
   float* part;         // PAIR: sum-of-squares partials [head*nparts + p][ldpart] (ldpart >= rows), NULL = none
   long ldpart;
@@ -61,28 +62,36 @@ struct GemmArgs {
   // order of the fp16 cross-attention within every step of 16 (position p of
   // a step holds width kperm_width(p)); requires hd % 16 == 0
   int qperm;
-  // REFINE: row r of batch (b1, b2) is candidate slot r of latent i = r / R;
-  // its key index is ridx[r] (< 0: empty).  The epilogue rotates by tab[key],
-  // dots with qex row i and writes (dot, sum of squares) partials.
-  const int* ridx;
-  long sI1, sI2;
-  const int* crow;     // REFINE: compacted work list, row r -> candidate slot crow[r] (batch strides sI1, sI2)
-  const int* mcount;   // optional per-batch row count (device), overrides M; tiles past it exit at once
-  int R;
-  const float* qex;
-  long ldqex, sE1, sE2;
-  float2* rpart;
-  long sR1, sR2;
   // RESID: optional per-row factor of the product, rowscale[row / rowscale_div]
   // (undoes the fp16 range scale of the value path per KV head)
   const float* rowscale;
   int rowscale_div;
+  // Output layout (STORE and PAIR): CTILE_NONE row-major (ldc); CTILE_KEYS the
+  // fragment-tiled key layout of the fp16 attention kernel, row r = h *
+  // ctile_rows + n, column c * hd + x -> ktile_off(h * ctile_heads + c, n, x,
+  // ctile_npad, hd); CTILE_VALUES its tiled value layout, row = feature f,
+  // column = key n -> xtile_off(0, f, n, ctile_npad) (per batch: sC1).
+  int ctile, ctile_heads;
+  long ctile_rows, ctile_npad;
   float scale;         // SCALE: C = acc * scale * rq[r] * rk[col]
   const float* rq;
   long ldrq, sQ1, sQ2;
   const float* rk;
   long ldrk, sK1, sK2;
 };
+
+// Element offset of output (row r, column col) in the layout g.ctile names.
+// Eight consecutive columns from a multiple of 8 stay contiguous in every
+// layout, so the epilogues' 16-byte runs keep their form.
+__device__ __forceinline__ long c_off(const GemmArgs& g, long r, long col) {
+  if (g.ctile == CTILE_KEYS) {
+    const long h = r / g.ctile_rows, n = r - h * g.ctile_rows;
+    const long c = col / g.hd, x = col - c * g.hd;
+    return ktile_off(h * g.ctile_heads + c, n, x, g.ctile_npad, g.hd);
+  }
+  if (g.ctile == CTILE_VALUES) return xtile_off(0, r, col, g.ctile_npad, 32);
+  return r * g.ldc + col;
+}
 
 __device__ __forceinline__ float silu_f(float x) { return x / (1.f + expf(-x)); }
 __device__ __forceinline__ float gelu_f(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
@@ -110,11 +119,16 @@ template <> __device__ __forceinline__ int lds_swz<8>(int r) { return ((r ^ (r >
 template <int BM, int BN, int BK, class CT>
 constexpr int gemm_lds_bytes() {
   const int ops = 2 * (BM + BN) * BK * (int)sizeof(CT);
-  const int stg = 4 * 32 * (BN / 2 + 8) * 4 + 2 * BM * 4;   // staging + REFINE row info
+  const int stg = 4 * 32 * (BN / 2 + 8) * 4;   // epilogue staging
   return ops > stg ? ops : stg;
 }
 
-template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK>
+// ST = 0: operands through registers into two LDS stages (any element types,
+// converted on the way), loaded two k steps ahead.  ST = 2: fp16 operands
+// copied straight from global memory into two LDS stages (global_load_lds,
+// 16 bytes a lane), the next k step in flight during the current one's MFMAs;
+// needs K % BK == 0 and 16-byte aligned rows and strides (host checks).
+template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK, int ST = 0>
 __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   typedef Mma<CT> MM;
   typedef typename MM::frag frag;
@@ -123,7 +137,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int TM = BM / 64, TN = BN / 64;    // 32x32 tiles per wave
   constexpr int KV = BK / E;                   // 16-byte vectors per tile row
   constexpr int AV = BM * KV / 256, BV = BN * KV / 256;
-  constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
+  constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU);
   static_assert(AV >= 1 && BV >= 1 && BM * KV % 256 == 0 && BN * KV % 256 == 0, "tile/threads");
   static_assert(TN % 2 == 0, "BN must allow two column halves per wave");
   // epilogue staging (per wave: 32 rows x TN*32 columns of fp32) must fit the arena
@@ -131,12 +145,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int SLD = WC + 8;                  // staging row stride (floats): rows r and r+4 on disjoint banks
   static_assert(WC == BN / 2, "wave column count");
   constexpr int LDSB = gemm_lds_bytes<BM, BN, BK, CT>();
+  constexpr int SS = (BM + BN) * LR;            // elements per stage: A rows, then B rows
   static_assert(4 * 32 * SLD * 4 <= LDSB, "staging does not fit");
 
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDSB];
   __shared__ float sc_f[EPI == EPI_SCALE ? BM + BN : 1];   // SCALE: row factors, then column factors
-  CT* As = (CT*)smem;                          // [2][BM*LR]
-  CT* Bs = As + 2 * BM * LR;                   // [2][BN*LR]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -169,12 +182,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   }
 
   const int bz = blockIdx.z, b1 = bz / g.nb2, b2 = bz - b1 * g.nb2;
-  const int M = g.mcount ? g.mcount[bz] : g.M;
-  // REFINE with a device-side row count: the grid holds fewer M tiles than
-  // the row bound and each workgroup walks M tiles mt0, mt0 + gridDim.y, ...
-  // (no launches of workgroups that would find no rows).  Other kernels take
-  // one tile per workgroup (and exit at once past a device-side row count).
-  for (int mt = mt0; (long)mt * BM < M; mt += gy) {
+  const int M = g.M;
+  {
+  const int mt = mt0;
   const TA* A = (const TA*)g.A + b1 * g.sA1 + b2 * g.sA2;
   const TB* B = (const TB*)g.B + b1 * g.sB1 + b2 * g.sB2;
   const TB* B2 = PAIRED && g.B2 ? (const TB*)g.B2 + b1 * g.sB1 + b2 * g.sB2 : nullptr;
@@ -206,28 +216,74 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     return rr < Mg;
   };
 
+  // LDS element offset of (row, 16-byte unit) in a stage
+  auto lds_at = [&](int r, int u) { return r * LR + ((u ^ lds_swz<KV>(r)) * E); };
+  // local LDS column of the wave's tile tn (two halves, same sub-range in each)
+  auto col_base = [&](int tn) {
+    const int half = tn / (TN / 2), i = tn % (TN / 2);
+    return half * (BN / 2) + wn * (BN / 4) + i * 32;
+  };
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int a = 0; a < TM; ++a)
+#pragma unroll
+    for (int b = 0; b < TN; ++b) acc[a][b] = zero16();
+  // B operand row of tile-local row lc (paired kinds: the pair members of
+  // the two column halves) and whether it lies inside the product
+  auto b_row = [&](int lc, bool& valid) -> const TB* {
+    if (PAIRED) {
+      const int half = lc / (BN / 2);
+      const int P = nt * (BN / 2) + (lc % (BN / 2));
+      valid = P < N;
+      if (EPI == EPI_PAIR) {
+        const int c = P / hh, j = P - c * hh;
+        return B + (long)(c * g.hd + j + half * hh) * g.ldb;
+      }
+      return (half ? B2 : B) + (long)P * g.ldb;
+    }
+    const int n = nt * BN + lc;
+    valid = n < N;
+    return B + (long)n * g.ldb;
+  };
+  // SCALE: the per-row and per-column factors (BM + BN values) are loaded
+  // together with the first k step's operands and kept in LDS for the
+  // epilogue, so their latency is not exposed after the k loop
+  float scf[(BM + BN + 255) / 256];
+  auto load_scale = [&]() {
+    if constexpr (EPI == EPI_SCALE) {
+      const float* rqv = g.rq + b1 * g.sQ1 + b2 * g.sQ2;
+      const float* rkv = g.rk + b1 * g.sK1 + b2 * g.sK2;
+#pragma unroll
+      for (int i = 0; i < (BM + BN + 255) / 256; ++i) {
+        const int v = tid + 256 * i;
+        float f = 0.f;
+        if (v < BM) {
+          const long r = grow(v);
+          if (r >= 0) f = rqv[r * g.ldrq];
+        } else if (v < BM + BN) {
+          const int col = nt * BN + (v - BM);
+          if (col < N) f = rkv[(long)col * g.ldrk] * g.scale;
+        }
+        scf[i] = f;
+      }
+    }
+  };
+  auto store_scale = [&]() {
+    if constexpr (EPI == EPI_SCALE) {
+#pragma unroll
+      for (int i = 0; i < (BM + BN + 255) / 256; ++i)
+        if (tid + 256 * i < BM + BN) sc_f[tid + 256 * i] = scf[i];
+    }
+  };
+  CT* smem_ct = (CT*)smem;
+  if constexpr (ST == 0) {
   // global -> register staging, two sets: loads run two k steps ahead
   frag ra[2][AV], rb[2][BV];
   const TB* brow_ptr[BV];
   bool bvalid[BV];
 #pragma unroll
   for (int i = 0; i < BV; ++i) {
-    const int v = tid + i * 256, lc = v / KV;
-    if (PAIRED) {
-      const int half = lc / (BN / 2);
-      const int P = nt * (BN / 2) + (lc % (BN / 2));
-      bvalid[i] = P < N;
-      if (EPI == EPI_PAIR || EPI == EPI_REFINE) {
-        const int c = P / hh, j = P - c * hh;
-        brow_ptr[i] = B + (long)(c * g.hd + j + half * hh) * g.ldb;
-      } else {
-        brow_ptr[i] = (half ? B2 : B) + (long)P * g.ldb;
-      }
-    } else {
-      const int n = nt * BN + lc;
-      bvalid[i] = n < N;
-      brow_ptr[i] = B + (long)n * g.ldb;
-    }
+    brow_ptr[i] = b_row((tid + i * 256) / KV, bvalid[i]);
     if (!bvalid[i]) brow_ptr[i] = B;   // loads always issue (from row 0) and are zeroed
   }
 
@@ -261,37 +317,25 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     for (int i = 0; i < BV; ++i) xb[i] = VecLoad<CT, TB>::load(brow_ptr[i] + gkb);
     return kin;
   };
-  // LDS element offset of (row, 16-byte unit) in a stage
-  auto lds_at = [&](int r, int u) { return r * LR + ((u ^ lds_swz<KV>(r)) * E); };
   const int su = tid % KV;
   auto store_stage = [&](int buf, const frag (&xa)[AV], const frag (&xb)[BV], bool kin) {
 #pragma unroll
     for (int i = 0; i < AV; ++i)
-      *(frag*)&As[buf * BM * LR + lds_at((tid + i * 256) / KV, su)] = (aoff[i] >= 0 && kin) ? xa[i] : zero_frag<CT>();
+      *(frag*)&smem_ct[buf * SS + lds_at((tid + i * 256) / KV, su)] = (aoff[i] >= 0 && kin) ? xa[i] : zero_frag<CT>();
 #pragma unroll
     for (int i = 0; i < BV; ++i)
-      *(frag*)&Bs[buf * BN * LR + lds_at((tid + i * 256) / KV, su)] = (bvalid[i] && kin) ? xb[i] : zero_frag<CT>();
+      *(frag*)&smem_ct[buf * SS + BM * LR + lds_at((tid + i * 256) / KV, su)] = (bvalid[i] && kin) ? xb[i] : zero_frag<CT>();
   };
 
-  // local LDS column of the wave's tile tn (two halves, same sub-range in each)
-  auto col_base = [&](int tn) {
-    const int half = tn / (TN / 2), i = tn % (TN / 2);
-    return half * (BN / 2) + wn * (BN / 4) + i * 32;
-  };
 
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int a = 0; a < TM; ++a)
-#pragma unroll
-    for (int b = 0; b < TN; ++b) acc[a][b] = zero16();
 
   // k steps past the end reload the last one (their data is never stored)
   auto issue = [&](int kn, frag (&xa)[AV], frag (&xb)[BV]) -> bool {
     return load_stage(kn < nk ? kn : nk - 1, xa, xb);
   };
   auto compute = [&](int buf) {
-    const CT* Ac = As + buf * BM * LR;
-    const CT* Bc = Bs + buf * BN * LR;
+    const CT* Ac = smem_ct + buf * SS;
+    const CT* Bc = Ac + BM * LR;
 #pragma unroll
     for (int ks = 0; ks < BK / (2 * E); ++ks) {
       frag af[TM], bfr[TN];
@@ -317,34 +361,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     if (kt + 1 < nk) store_stage((kt + 1) & 1, na, nb, nkin);
     __syncthreads();
   };
-  // SCALE: the per-row and per-column factors (BM + BN values) are loaded
-  // together with the first k step's operands and kept in LDS for the
-  // epilogue, so their latency is not exposed after the k loop
-  float scf[(BM + BN + 255) / 256];
-  if constexpr (EPI == EPI_SCALE) {
-    const float* rqv = g.rq + b1 * g.sQ1 + b2 * g.sQ2;
-    const float* rkv = g.rk + b1 * g.sK1 + b2 * g.sK2;
-#pragma unroll
-    for (int i = 0; i < (BM + BN + 255) / 256; ++i) {
-      const int v = tid + 256 * i;
-      float f = 0.f;
-      if (v < BM) {
-        const long r = grow(v);
-        if (r >= 0) f = rqv[r * g.ldrq];
-      } else if (v < BM + BN) {
-        const int col = nt * BN + (v - BM);
-        if (col < N) f = rkv[(long)col * g.ldrk] * g.scale;
-      }
-      scf[i] = f;
-    }
-  }
+  load_scale();
   kin0 = issue(0, ra[0], rb[0]);
   store_stage(0, ra[0], rb[0], kin0);
-  if constexpr (EPI == EPI_SCALE) {
-#pragma unroll
-    for (int i = 0; i < (BM + BN + 255) / 256; ++i)
-      if (tid + 256 * i < BM + BN) sc_f[tid + 256 * i] = scf[i];
-  }
+  store_scale();
   kin1 = issue(1, ra[1], rb[1]);
   __syncthreads();
   int kt = 0;
@@ -353,6 +373,83 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     step(kt + 1, ra[1], rb[1], kin1, ra[0], rb[0], kin0);
   }
   if (kt < nk) step(kt, ra[0], rb[0], kin0, ra[1], rb[1], kin1);
+  } else {
+  // ---- direct global -> LDS loads into the two stages.  One wave instruction
+  // fills one 1 KB block of a stage (RPB tile rows); lane l writes unit l % KV
+  // of row l / KV and so reads the global unit that the swizzle puts there.
+  // Rows past the end read row 0: they only reach outputs that are not stored.
+  static_assert(sizeof(CT) == 2 && sizeof(TA) == 2 && sizeof(TB) == 2, "direct loads copy fp16 operands");
+  constexpr int RPB = 512 / BK;                 // tile rows per 1 KB block
+  constexpr int NBLK = (BM + BN) / RPB;         // blocks per stage
+  constexpr int NI = NBLK / 4;                  // blocks per wave and stage
+  static_assert(NBLK % 4 == 0 && BM % RPB == 0 && ST == 2, "direct load blocks");
+  const int w = __builtin_amdgcn_readfirstlane(wave);
+  const int nk = K / BK;
+  const CT* src[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int rho = (i * 4 + w) * RPB + lane / KV;
+    const int u = (lane % KV) ^ lds_swz<KV>(rho);   // rho and rho - BM agree mod 16
+    if (rho < BM) {
+      const long gr = grow(rho);
+      src[i] = (const CT*)A + (gr >= 0 ? gr * g.lda : 0) + u * E;
+    } else {
+      bool valid;
+      const TB* bp = b_row(rho - BM, valid);
+      src[i] = (const CT*)(valid ? bp : B) + u * E;
+    }
+  }
+  // k step kn into stage kn % 2
+  auto dma = [&](int kn) {
+    CT* st = smem_ct + (kn & 1) * SS;
+    const long ks = (long)kn * BK;
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(src[i] + ks),
+                                       (__attribute__((address_space(3))) void*)(st + (i * 4 + w) * 512), 16, 0, 0);
+  };
+  // this wave's loads of all but the newest n k steps have landed and its
+  // LDS reads have completed (vmcnt(n * NI), lgkmcnt(0)); the compiler
+  // tracks neither across the barrier that follows
+  auto wait_steps = [&](auto n) {
+    constexpr int c = decltype(n)::value * NI;
+    __builtin_amdgcn_s_waitcnt((c & 15) | ((c >> 4) << 14) | 0x70);
+  };
+  auto compute = [&](const CT* Ac) {
+    const CT* Bc = Ac + BM * LR;
+    constexpr int KS = BK / (2 * E);
+    frag af[2][TM], bfr[2][TN];
+    auto rd = [&](int ks, int p) {
+#pragma unroll
+      for (int a = 0; a < TM; ++a) af[p][a] = *(const frag*)&Ac[lds_at(wm * (BM / 2) + a * 32 + l32, ks * 2 + lg)];
+#pragma unroll
+      for (int b = 0; b < TN; ++b) bfr[p][b] = *(const frag*)&Bc[lds_at(col_base(b) + l32, ks * 2 + lg)];
+    };
+    rd(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) rd(ks + 1, (ks + 1) & 1);   // next fragments in flight during this step's MFMAs
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int a = 0; a < TM; ++a)
+#pragma unroll
+        for (int b = 0; b < TN; ++b) MM::mma(acc[a][b], af[ks & 1][a], bfr[ks & 1][b]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  dma(0);
+  load_scale();
+  store_scale();
+  wait_steps(std::integral_constant<int, 0>());
+  __builtin_amdgcn_s_barrier();
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) dma(kt + 1);   // stage (kt + 1) % 2 was released by the last barrier
+    __builtin_amdgcn_sched_barrier(0);
+    compute(smem_ct + (kt & 1) * SS);
+    wait_steps(std::integral_constant<int, 0>());
+    __builtin_amdgcn_s_barrier();
+  }
+  }
 
   // ------------------------------------------------------------------ epilogue
   // Per 32-row slice a of the wave's block: values -> LDS staging (fp32, the
@@ -365,7 +462,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   TC* C = (TC*)g.C + b1 * g.sC1 + b2 * g.sC2;
   const TBias* bias = g.bias ? (const TBias*)g.bias + b2 * g.sBias2 : nullptr;
   const int P0 = nt * (BN / 2) + wn * (BN / 4);           // first pair of the wave (paired kinds)
-  const int pc = PAIRED ? P0 / (hh > 0 ? hh : 1) : 0;     // head of the wave's pairs (PAIR, REFINE)
+  const int pc = PAIRED ? P0 / (hh > 0 ? hh : 1) : 0;     // head of the wave's pairs (PAIR)
   const int pj0 = PAIRED ? P0 - pc * hh : 0;
   constexpr int RUN = BN / 4;
   // columns of run q, element x: global output column and validity
@@ -374,23 +471,6 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     else if constexpr (EPI == EPI_SWIGLU) return (long)P0 + x;
     else return (long)nt * BN + q * (BN / 2) + wn * (BN / 4) + x;
   };
-
-  const int* ridx = (EPI == EPI_REFINE) ? g.ridx + b1 * g.sI1 + b2 * g.sI2 : nullptr;
-  const int* crow = (EPI == EPI_REFINE && g.crow) ? g.crow + b1 * g.sI1 + b2 * g.sI2 : nullptr;
-  // REFINE: slot and key of every tile row, read once into LDS (after the
-  // staging area) instead of per element
-  int* rslot = (int*)((float*)smem + 4 * 32 * SLD);
-  int* rkey = rslot + BM;
-  if constexpr (EPI == EPI_REFINE) {
-    for (int lr = tid; lr < BM; lr += 256) {
-      const long r = grow(lr);
-      const int slot = r < 0 ? 0 : (crow ? crow[r] : (int)r);
-      rslot[lr] = slot;
-      const int key = r < 0 ? -1 : ridx[slot];
-      rkey[lr] = key < 0 ? 0 : key;
-    }
-    __syncthreads();
-  }
 
 #pragma unroll
   for (int a = 0; a < TM; ++a) {
@@ -439,7 +519,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
           const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
           stg[rl * SLD + b * 32 + l32] = silu_f(acc[a][b][j]) * acc[a][b + TN / 2][j];
         }
-    } else {   // PAIR, REFINE: biased pair members; rotation in the vector pass
+    } else {   // PAIR: biased pair members; rotation in the vector pass
 #pragma unroll
       for (int b = 0; b < TN / 2; ++b) {
         const int x = b * 32 + l32;                 // position in the wave's run
@@ -456,14 +536,14 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       }
     }
     wave_lds_fence();
-    if constexpr (EPI == EPI_PAIR || EPI == EPI_REFINE) {
+    if constexpr (EPI == EPI_PAIR) {
       // ---- 2p. pairs: 8 pairs per lane and step, rows split over NV lanes.
       // Rotation by the table row, 16-byte stores of both members, the
-      // row's sum of squares (rotation keeps it) and, for REFINE, the dot
-      // product with the query row; both reduced over the NV lanes of a row.
+      // row's sum of squares (rotation keeps it), reduced over the NV lanes
+      // of a row.
       constexpr int PV = 8, NV = RUN / PV;
       static_assert(NV >= 1 && 64 % NV == 0 && (32 * NV) % 64 == 0, "pair vector pass");
-      const bool want_ss = (EPI == EPI_REFINE) || g.part != nullptr;
+      const bool want_ss = g.part != nullptr;
       const int nparts = (hh / (BN / 2)) * 2;
       const int pidx = (pj0 / (BN / 2)) * 2 + wn;
 #pragma unroll
@@ -474,7 +554,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
         const bool rok = grow2(lbase + rl, rgrp, rrow);
         const long r = rok ? (long)rgrp * g.mgstride + rrow : -1;
         const int nvalid = N - (P0 + vx);
-        float sp = 0.f, dp = 0.f;
+        float sp = 0.f;
         if (rok && nvalid > 0) {
           float v0[PV], v1[PV];
           const float* s0 = stg + rl * SLD + vx;
@@ -492,9 +572,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
           for (int u = 0; u < PV; ++u) sp += v0[u] * v0[u] + v1[u] * v1[u];
           const int jp = pj0 + vx;
           if (g.tab) {
-            int trow;
-            if constexpr (EPI == EPI_REFINE) trow = rkey[lbase + rl];
-            else trow = (mg > 1 && g.mgstride == g.tab_mod) ? rrow : (int)r % g.tab_mod;
+            const int trow = (mg > 1 && g.mgstride == g.tab_mod) ? rrow : (int)r % g.tab_mod;
             const float2* tp = g.tab + (long)trow * hh + jp;
 #pragma unroll
             for (int u = 0; u < PV; u += 2) {
@@ -508,17 +586,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
             }
           }
           const long col0 = (long)pc * g.hd + jp;
-          if constexpr (EPI == EPI_REFINE) {
-            const float* qe = g.qex + b1 * g.sE1 + b2 * g.sE2 + (long)(rslot[lbase + rl] / g.R) * g.ldqex + col0;
-#pragma unroll
-            for (int u = 0; u < PV; u += 4) {
-              const f32x4 q0 = *(const f32x4*)(qe + u);
-              const f32x4 q1 = *(const f32x4*)(qe + hh + u);
-#pragma unroll
-              for (int w = 0; w < 4; ++w) dp += v0[u + w] * q0[w] + v1[u + w] * q1[w];
-            }
-          } else {
-            TC* d0 = C + r * g.ldc + col0;
+          {
+            TC* d0 = C + c_off(g, r, col0);
+            TC* d1 = C + c_off(g, r, col0 + hh);
             constexpr int VE = Vec16<TC>::n;
             const bool vec_ok = nvalid >= PV && (g.ldc % VE) == 0 && (((uintptr_t)C & 15) == 0);
             float s0[PV], s1[PV];   // values in store order
@@ -552,12 +622,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
                   t1[w] = from_f32<TC>(s1[u + w]);
                 }
                 *(uint4*)(d0 + u) = *(const uint4*)t0;
-                *(uint4*)(d0 + hh + u) = *(const uint4*)t1;
+                *(uint4*)(d1 + u) = *(const uint4*)t1;
               }
             } else {
               for (int u = 0; u < PV && u < nvalid; ++u) {
                 d0[u] = from_f32<TC>(s0[u]);
-                d0[hh + u] = from_f32<TC>(s1[u]);
+                d1[u] = from_f32<TC>(s1[u]);
               }
             }
             if (g.C2) {
@@ -579,18 +649,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
         }
         if (want_ss) {
 #pragma unroll
-          for (int o = 1; o < NV; o <<= 1) {
-            sp += __shfl_xor(sp, o);
-            if constexpr (EPI == EPI_REFINE) dp += __shfl_xor(dp, o);
-          }
-          if ((e % NV) == 0 && rok) {
-            if constexpr (EPI == EPI_REFINE) {
-              float2* rp = g.rpart + b1 * g.sR1 + b2 * g.sR2;
-              rp[(long)rslot[lbase + rl] * nparts + pidx] = make_float2(dp, sp);
-            } else {
-              g.part[(long)(pc * nparts + pidx) * g.ldpart + r] = sp;   // partial-major: rows contiguous
-            }
-          }
+          for (int o = 1; o < NV; o <<= 1) sp += __shfl_xor(sp, o);
+          if ((e % NV) == 0 && rok)
+            g.part[(long)(pc * nparts + pidx) * g.ldpart + r] = sp;   // partial-major: rows contiguous
         }
       }
     } else {
@@ -648,7 +709,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
         if (r < 0) continue;
         const float* src = stg + rl * SLD + q * RUN + vx;
         const long col = run_col(q, vx);
-        TC* dst = C + r * g.ldc + col;
+        TC* dst = C + c_off(g, r, col);
         int nvalid;
         if constexpr (PAIRED) {
           nvalid = N - (P0 + vx);
@@ -677,22 +738,18 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     }
     wave_lds_fence();
   }
-  if constexpr (EPI != EPI_REFINE) break;   // one tile per workgroup
-  if (!g.mcount) break;
-  __syncthreads();        // LDS (staging, row info) is reused by the next tile
-  }  // M tile loop
+  }  // tile
 }
 
-template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK>
+template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK, int ST = 0>
 hipError_t launch_gemm(const GemmArgs& g, int batch, hipStream_t st) {
-  constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
+  constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU);
   const int ntn = PAIRED ? (g.N + BN / 2 - 1) / (BN / 2) : (g.N + BN - 1) / BN;
   const int mg = g.mgroups > 1 ? g.mgroups : 1;
-  int ntm = mg == 1 ? (g.M + BM - 1) / BM : (g.M / mg + BM / mg - 1) / (BM / mg);
-  if (EPI == EPI_REFINE && g.mcount && ntm > 8) ntm = 8;   // device-side row count: workgroups loop over M tiles
+  const int ntm = mg == 1 ? (g.M + BM - 1) / BM : (g.M / mg + BM / mg - 1) / (BM / mg);
   if (ntn <= 0 || ntm <= 0 || batch <= 0) return hipSuccess;
   dim3 grid(ntn, ntm, batch);
-  hipLaunchKernelGGL((gemm_kernel<CT, TA, TB, TC, TBias, EPI, BM, BN, BK>), grid, dim3(256), 0, st, g);
+  hipLaunchKernelGGL((gemm_kernel<CT, TA, TB, TC, TBias, EPI, BM, BN, BK, ST>), grid, dim3(256), 0, st, g);
   return hipGetLastError();
 }
 

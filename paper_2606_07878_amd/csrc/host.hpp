@@ -135,6 +135,13 @@ struct Dims {
   int att_tt;           // latents per attention workgroup
   int splits;           // split-N factor of the cross-attention
   long keys_per_split;
+  // latent self-attention on the fp16 flash kernel (bf16 mode, d_s of 128,
+  // 256 or 512): keys and values in its tiled layouts with tpadk keys per
+  // head, split over sa_splits key ranges; otherwise scores, softmax and
+  // product as separate passes
+  bool sa_flash;
+  int tpadk, sa_splits;
+  long sa_kps;
   size_t cs;            // bytes of the compute/storage type
   bool fp32;
 };
@@ -151,6 +158,7 @@ struct Plan {
   size_t k, partk, rk, opart, mpart, lpart;
   // ... or self-attention / FFN buffers
   size_t qs, ks, vT, partqs, partks, rqs, rks, Ssa, Psa, Osa, hid;
+  size_t opart_s, mpart_s, lpart_s;   // flash self-attention partials
   size_t total;
 };
 
@@ -220,6 +228,20 @@ inline still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims*
   m->splits = choose_splits(*m);
   m->keys_per_split = rup((m->N + m->splits - 1) / m->splits, key_block(*m));
   m->splits = (int)((m->N + m->keys_per_split - 1) / m->keys_per_split);
+  m->tpadk = (int)rup(t, XATT_KB);
+  m->sa_flash = !m->fp32 && m->ns > 0 && (m->ds == 128 || m->ds == 256 || m->ds == 512) &&
+                (double)m->tpadk * m->Es * 2.0 < 4294967296.0;
+  m->sa_splits = 1;
+  m->sa_kps = m->tpadk;
+  if (m->sa_flash) {
+    const int tt = m->ds <= 256 ? 128 : 64;
+    const long wgs = (long)((t + tt - 1) / tt) * m->H * m->ns;
+    long s = (512 + wgs - 1) / wgs;
+    if (s > m->tpadk / XATT_KB) s = m->tpadk / XATT_KB;
+    if (s < 1) s = 1;
+    m->sa_kps = rup((t + s - 1) / s, XATT_KB);
+    m->sa_splits = (int)((t + m->sa_kps - 1) / m->sa_kps);
+  }
   return STILL_OK;
 }
 
@@ -276,7 +298,7 @@ inline int stage_rows(const Dims& m) {
 inline int stage_blocks(const Dims& m) { return (int)((m.Npad + stage_rows(m) - 1) / stage_rows(m)); }
 
 inline Plan make_plan(const still_config* c, const Dims& m) {
-  Plan p;
+  Plan p = {};
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
@@ -336,15 +358,23 @@ inline Plan make_plan(const still_config* c, const Dims& m) {
   off = ubase;
   if (m.ns > 0) {
     p.qs = take(cs * Ht * m.Es);
-    p.ks = take(cs * Ht * m.Es);
-    p.vT = take(cs * (size_t)m.H * m.Es * m.tpad);
     p.partqs = take(4ul * Ht * m.ns * m.np_s);
     p.partks = take(4ul * Ht * m.ns * m.np_s);
     p.rqs = take(4ul * Ht * m.ns);
     p.rks = take(4ul * Ht * m.ns);
-    p.Ssa = take(4ul * (size_t)m.H * m.ns * m.t * m.tpad);
-    p.Psa = take(cs * (size_t)m.H * m.ns * m.t * m.tpad);
     p.Osa = take(cs * Ht * m.Es);
+    if (m.sa_flash) {   // tiled keys and values, split partials
+      p.ks = take(cs * (size_t)m.H * m.tpadk * m.Es);
+      p.vT = take(cs * (size_t)m.H * m.Es * m.tpadk);
+      p.opart_s = take(4ul * m.sa_splits * Ht * m.Es);
+      p.mpart_s = take(4ul * m.sa_splits * Ht * m.ns);
+      p.lpart_s = take(4ul * m.sa_splits * Ht * m.ns);
+    } else {
+      p.ks = take(cs * Ht * m.Es);
+      p.vT = take(cs * (size_t)m.H * m.Es * m.tpad);
+      p.Ssa = take(4ul * (size_t)m.H * m.ns * m.t * m.tpad);
+      p.Psa = take(cs * (size_t)m.H * m.ns * m.t * m.tpad);
+    }
   }
   p.hid = take(cs * Ht * (m.F > 0 ? m.F : 1));
   p.total = (off > end1 ? off : end1) + 256;

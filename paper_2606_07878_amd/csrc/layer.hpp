@@ -23,6 +23,26 @@ template <> struct Tile<float> { static constexpr int BM = 128, BN = GEMM_BN, BK
 // workgroups fit a CU.
 constexpr int GEMM_LONG_K = 512;
 
+// Direct global -> LDS operand loads (two LDS stages, the next k step's copy
+// in flight during the current one's MFMAs; bit-identical results) apply to fp16
+// operands with whole k steps, 16-byte aligned rows and batch strides and no
+// split or wrapped operand; paired kinds also need whole runs of 8 pairs.
+static bool direct_ok(const GemmArgs& g, int bk, bool paired) {
+  auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  return g.K % bk == 0 && !g.A2 && !g.bwrap && g.lda % 8 == 0 && g.ldb % 8 == 0 && g.sA1 % 8 == 0 &&
+         g.sA2 % 8 == 0 && g.sB1 % 8 == 0 && g.sB2 % 8 == 0 && (g.mgroups <= 1 || g.mgstride % 8 == 0) && al(g.A) &&
+         al(g.B) && (!g.B2 || al(g.B2)) && (!paired || g.N % 8 == 0);
+}
+
+template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK>
+static hipError_t launch_pick(const GemmArgs& g, int batch, hipStream_t st) {
+  if constexpr (std::is_same<CT, f16>::value && std::is_same<TA, f16>::value && std::is_same<TB, f16>::value) {
+    if (direct_ok(g, BK, EPI == EPI_PAIR || EPI == EPI_SWIGLU))
+      return launch_gemm<CT, TA, TB, TC, TBias, EPI, BM, BN, BK, 2>(g, batch, st);
+  }
+  return launch_gemm<CT, TA, TB, TC, TBias, EPI, BM, BN, BK>(g, batch, st);
+}
+
 // WIDE: 128 x 256 tiles (BK 32, 2 waves per SIMD) for the latent-side
 // products with many output columns and K >= 512 (fp16 mode; paired kinds need
 // head widths that are multiples of 256), where they still leave at least two
@@ -32,25 +52,25 @@ template <class CT, class TA, class TB, class TC, class TBias, int EPI, bool WID
 static hipError_t gemm(const GemmArgs& g, int batch, hipStream_t st, int cls = STILL_K_LATENT) {
   timing::Scope ts(cls, st);
   if constexpr (WIDE && sizeof(CT) == 2) {
-    constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU || EPI == EPI_REFINE);
+    constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU);
     const long ntn = PAIRED ? (g.N + 127) / 128 : (g.N + 255) / 256;
     const long ntm = g.mgroups > 1 ? (g.M / g.mgroups + 128 / g.mgroups - 1) / (128 / g.mgroups) : (g.M + 127) / 128;
-    if (PAIRED || ntn * ntm * batch >= 512) return launch_gemm<CT, TA, TB, TC, TBias, EPI, 128, 256, 32>(g, batch, st);
+    if (PAIRED || ntn * ntm * batch >= 512) return launch_pick<CT, TA, TB, TC, TBias, EPI, 128, 256, 32>(g, batch, st);
   }
-  if constexpr (sizeof(CT) == 2 && EPI != EPI_REFINE) {
+  if constexpr (sizeof(CT) == 2) {
     // fewer 128-row tiles than CUs (the output heads, small t): 64-row tiles
     constexpr bool PAIRED = (EPI == EPI_PAIR || EPI == EPI_SWIGLU);
     const long ntn = PAIRED ? (g.N + 63) / 64 : (g.N + 127) / 128;
     const long ntm = g.mgroups > 1 ? (g.M / g.mgroups + 128 / g.mgroups - 1) / (128 / g.mgroups) : (g.M + 127) / 128;
     if (g.mgroups <= 1 && ntn * ntm * batch < 256) {
       if (g.K >= GEMM_LONG_K)
-        return launch_gemm<CT, TA, TB, TC, TBias, EPI, 64, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
-      return launch_gemm<CT, TA, TB, TC, TBias, EPI, 64, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
+        return launch_pick<CT, TA, TB, TC, TBias, EPI, 64, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
+      return launch_pick<CT, TA, TB, TC, TBias, EPI, 64, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
     }
   }
   if (g.K >= GEMM_LONG_K)
-    return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
-  return launch_gemm<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
+    return launch_pick<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, 2 * Tile<CT>::BK>(g, batch, st);
+  return launch_pick<CT, TA, TB, TC, TBias, EPI, Tile<CT>::BM, Tile<CT>::BN, Tile<CT>::BK>(g, batch, st);
 }
 
 static GemmArgs gargs(int M, int N, int K, const void* A, long lda, const void* B, long ldb, void* C, long ldc) {
@@ -70,14 +90,14 @@ static GemmArgs gargs(int M, int N, int K, const void* A, long lda, const void* 
 }
 
 
-template <class CT, int D2>
+template <class CT, int D2, int TOPK = XATT_TOPK>
 static hipError_t launch_attn(const AttnArgs& a, int splits, hipStream_t st) {
   dim3 grid((a.t + ATT_TT - 1) / ATT_TT, a.H * a.nc, splits);
   if constexpr (sizeof(CT) == 2) {
     constexpr int TT = D2 <= 256 ? 128 : 64;
     const int ntt = (a.t + TT - 1) / TT;
     static_assert(xatt_waves(D2) == 4, "the fp16 kernel runs 4 waves");
-    hipLaunchKernelGGL((xattn_f16_kernel<TT, D2, XATT_TOPK>), dim3(ntt * a.H * a.nc * splits), dim3(256), 0, st, a);
+    hipLaunchKernelGGL((xattn_f16_kernel<TT, D2, TOPK>), dim3(ntt * a.H * a.nc * splits), dim3(256), 0, st, a);
   } else {
     hipLaunchKernelGGL((cross_attn_kernel<CT, ATT_TT, (D2 > 256 ? 32 : ATT_NB), 32, D2, ATT_TOPK>), grid, dim3(256),
                        0, st, a);
@@ -304,6 +324,8 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
         a.cval = (float*)(ws + p.cval);
         a.cidx = (int*)(ws + p.cidx);
         a.ocnt = m.fp32 ? nullptr : (int*)(ws + p.ocnt);
+        a.xfeat = m.d2;
+        a.xcoff = 0;
         hipError_t e;
         {
         TIMED(STILL_K_CROSS_ATTN);
@@ -451,7 +473,103 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
       }
     }
     // ---------------- latent self-attention: Z += SelfAttn(RMSNorm(Z))
-    if (m.ns > 0) {
+    // bf16 mode, d_s of 128, 256 or 512: q row-major, k and v written by their
+    // projections straight into the fp16 flash kernel's tiled layouts, the
+    // flash kernel without logit refinement, then the split merge
+    if constexpr (sizeof(CT) == 2) {
+      if (m.ns > 0 && m.sa_flash) {
+        CT* qs = (CT*)(ws + p.qs);
+        CT* ks = (CT*)(ws + p.ks);
+        CT* vT = (CT*)(ws + p.vT);
+        float* partqs = (float*)(ws + p.partqs);
+        float* partks = (float*)(ws + p.partks);
+        float* rqs = (float*)(ws + p.rqs);
+        float* rks = (float*)(ws + p.rks);
+        CT* Osa = (CT*)(ws + p.Osa);
+        HIP_TRY(rmsnorm());
+        {
+          GemmArgs g = gargs((int)Ht, m.Es / 2, m.D, Y, m.D, bw.sa_wq, m.D, qs, m.Es);
+          g.bias = bw.sa_bq;
+          g.hd = m.ds;
+          g.part = partqs;
+          g.ldpart = Ht;
+          if (wide_s) HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR, true>(g, 1, st)));
+          else HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
+          g.B = bw.sa_wk;
+          g.bias = bw.sa_bk;
+          g.C = ks;
+          g.part = partks;
+          g.ctile = CTILE_KEYS;   // [h * n_s + c][key tiles]
+          g.ctile_rows = m.t;
+          g.ctile_heads = m.ns;
+          g.ctile_npad = m.tpadk;
+          if (wide_s) HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR, true>(g, 1, st)));
+          else HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
+        }
+        {  // v^T[h] = W_V^sa Y[h]^T, tiled [h][feature tiles][key steps]
+          GemmArgs g = gargs(m.Es, m.t, m.D, bw.sa_wv, m.D, Y, m.D, vT, m.tpadk);
+          g.sB1 = (long)m.t * m.D;
+          g.sC1 = (long)m.Es * m.tpadk;
+          g.ctile = CTILE_VALUES;
+          g.ctile_npad = m.tpadk;
+          HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_STORE, true>(g, m.H, st)));
+          if (m.tpadk > m.t) {   // keys past t: zero values (their weights are exactly 0)
+            TIMED(STILL_K_OTHER);
+            hipLaunchKernelGGL(zero_xtile_tail_kernel, dim3(grid1d((long)m.H * m.Es * (m.tpadk - m.t))), dim3(256), 0,
+                               st, (f16*)vT, (long)m.H * m.Es, m.t, m.tpadk);
+            HIP_TRY(hipGetLastError());
+          }
+        }
+        HIP_TRY(finalize(partqs, Ht, m.ns, wide_s ? m.ds / 256 * 2 : m.np_s, rqs));
+        HIP_TRY(finalize(partks, Ht, m.ns, wide_s ? m.ds / 256 * 2 : m.np_s, rks));
+        AttnArgs a;
+        memset(&a, 0, sizeof a);
+        a.q = qs;
+        a.ldq = m.Es;
+        a.rq = rqs;
+        a.k = ks;
+        a.rk = rks;
+        a.xt = vT;
+        a.npad = m.tpadk;
+        a.xfeat = m.Es;
+        a.xcoff = m.ds;
+        a.opart = (float*)(ws + p.opart_s);
+        a.mpart = (float*)(ws + p.mpart_s);
+        a.lpart = (float*)(ws + p.lpart_s);
+        a.H = m.H;
+        a.N = m.t;
+        a.t = m.t;
+        a.nc = m.ns;
+        a.dc = m.ds;
+        a.d2 = m.ds;
+        a.scale_log2 = (cfg->logit_scale_self != 0.f ? cfg->logit_scale_self : (float)m.ds) * LOG2E;
+        a.keys_per_split = (int)m.sa_kps;
+        RefineArgs ra;
+        memset(&ra, 0, sizeof ra);
+        {
+          TIMED(STILL_K_LATENT);
+          hipError_t e;
+          if (m.ds == 128) e = launch_attn<CT, 128, 0>(a, m.sa_splits, st);
+          else if (m.ds == 256) e = launch_attn<CT, 256, 0>(a, m.sa_splits, st);
+          else e = launch_attn<CT, 512, 0>(a, m.sa_splits, st);
+          HIP_TRY(e);
+          const dim3 mg((unsigned)((Ht * m.ns + 3) / 4));
+          if (m.ds == 128)
+            hipLaunchKernelGGL((merge_kernel<CT, 2>), mg, dim3(256), 0, st, a.opart, a.mpart, a.lpart, m.sa_splits,
+                               m.H, m.ns, m.t, Osa, ra);
+          else if (m.ds == 256)
+            hipLaunchKernelGGL((merge_kernel<CT, 4>), mg, dim3(256), 0, st, a.opart, a.mpart, a.lpart, m.sa_splits,
+                               m.H, m.ns, m.t, Osa, ra);
+          else
+            hipLaunchKernelGGL((merge_kernel<CT, 8>), mg, dim3(256), 0, st, a.opart, a.mpart, a.lpart, m.sa_splits,
+                               m.H, m.ns, m.t, Osa, ra);
+          HIP_TRY(hipGetLastError());
+        }
+        GemmArgs g = gargs((int)Ht, m.D, m.Es, Osa, m.Es, bw.sa_wo, m.Es, Z, m.D);
+        HIP_TRY((gemm<CT, CT, CT, float, IT, EPI_RESID, true>(g, 1, st)));
+      }
+    }
+    if (m.ns > 0 && !m.sa_flash) {
       CT* qs = (CT*)(ws + p.qs);
       CT* ks = (CT*)(ws + p.ks);
       CT* vT = (CT*)(ws + p.vT);

@@ -703,6 +703,17 @@ __global__ void zero_cols_kernel(T* __restrict__ A, long rows, int ld, int c0, i
   }
 }
 
+// Zero keys [t, npad) of rows feature-major values in the tiled layout
+// (xtile_off): rows = (KV heads) x (features per head), npad keys per row.
+static __global__ void zero_xtile_tail_kernel(f16* __restrict__ A, long rows, int t, long npad) {
+  const long w = npad - t;
+  const long total = rows * w;
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    const long r = i / w;
+    A[xtile_off(0, r, t + (i - r * w), npad, 32)] = (f16)0.f;
+  }
+}
+
 // Element-type conversion of up to CONV_SEGS weight matrices per launch
 // (bf16 -> fp16 for the MFMA operands), one segment per grid row, 8 elements
 // per thread and step; segment lengths are multiples of 8 and 16-byte aligned.
