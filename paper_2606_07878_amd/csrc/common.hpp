@@ -142,6 +142,28 @@ template <class CT> __device__ __forceinline__ typename Mma<CT>::frag zero_frag(
   return z;
 }
 
+// (cos, sin) of the RoPE angle pos * inv.  The angle is formed in fp64 and
+// reduced there to x = angle - q pi/2 with |x| <= pi/4 (pi/2 in two parts);
+// sin x and cos x come from their Taylor series in fp32 (the first omitted
+// terms are below 3e-8 on |x| <= pi/4), then the quadrant q mod 4 picks the
+// signs and the order.
+__device__ __forceinline__ float2 rope_cs(double pos, double inv) {
+  const double ang = pos * inv;
+  const double q = rint(ang * 0.63661977236758134);
+  double r = fma(-q, 1.5707963267948966, ang);
+  r = fma(-q, 6.123233995736766e-17, r);
+  const float x = (float)r, x2 = x * x;
+  const float s = fmaf(x * x2, -1.f / 6 + x2 * (1.f / 120 + x2 * (-1.f / 5040 + x2 * (1.f / 362880))), x);
+  const float c = fmaf(x2, -0.5f + x2 * (1.f / 24 + x2 * (-1.f / 720 + x2 * (1.f / 40320))), 1.f);
+  // quadrant k = q mod 4 (exact in fp64); branch-free: odd k swaps the two
+  // values, k in {1, 2} negates the cosine, k in {2, 3} the sine
+  const int k = (int)(q - 4.0 * floor(q * 0.25));
+  const bool swap = k & 1;
+  const uint32_t nc = (uint32_t)((k + 1) & 2) << 30, ns = (uint32_t)(k & 2) << 30;
+  return make_float2(__uint_as_float(__float_as_uint(swap ? s : c) ^ nc),
+                     __uint_as_float(__float_as_uint(swap ? c : s) ^ ns));
+}
+
 __device__ __forceinline__ f32x16 zero16() {
   f32x16 z;
 #pragma unroll

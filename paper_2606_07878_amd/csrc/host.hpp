@@ -309,7 +309,10 @@ inline Plan make_plan(const still_config* c, const Dims& m) {
   const long Ht = (long)m.H * m.t;
   const long HN = (long)m.H * m.N;
   p.pq = take(sizeof(double) * m.t);
-  p.tab_ck = take(8ul * m.N * (m.dc / 2));
+  // compactor-RoPE table of the keys: fp32 mode only (bf16 mode: rotations
+  // computed in place from the positions and the fp64 frequencies)
+  p.tab_ck = m.fp32 ? take(8ul * m.N * (m.dc / 2)) : 0;
+  p.invf_c = take(8ul * (m.dc / 2));
   p.tab_cq = take(8ul * m.t * (m.dc / 2));
   p.tab_bk = take(8ul * m.N * (m.d / 2));
   p.tab_bq = take(8ul * m.t * (m.d / 2));
@@ -341,7 +344,6 @@ inline Plan make_plan(const still_config* c, const Dims& m) {
     if (m.fp32) {
       p.q64 = take(8ul * Ht * m.Ec);
       p.invf_b = take(8ul * (m.d / 2));
-      p.invf_c = take(8ul * (m.dc / 2));
     }
     p.crow = take(4ul * HCT * m.R);
     p.ccount = take(4ul * m.H * m.nc);

@@ -53,7 +53,8 @@ struct KprojArgs {
   const f16* X;         // [H*N][d2] RoPE-fixed keys and values
   const f16* wkt;       // W_K fragment-tiled (wtile_off), nc*dc rows
   const void* bias;     // [nc*dc] b_K (TBias) or NULL
-  const float2* tab;    // [N][dc/2] (cos, sin) of the compactor RoPE at the key positions
+  const double* pos;    // [N] key positions
+  const double* invf;   // [dc/2] compactor RoPE frequencies (fp64)
   f16* k;               // tiled keys (ktile_off with npad keys per head), permuted widths
   float* part;          // [nc][H*N] sum of squares of k~ (one partial per row and cross head)
   const float* hscale;  // [H] fp16 range scale of the staged X of each KV head (the bias is scaled with it), or NULL
@@ -92,12 +93,18 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
     if (h < a.H && n < a.N) val = *(const uint4*)(a.X + ((long)h * a.N + n) * D2 + col);
     *(uint4*)&Xs[r * LX + col] = val;
   }
-  auto load_tab = [&](int p, int buf) {   // table rows n0 .. n0 + kpw - 1, pairs 32p .. 32p + 31
+  // rotation tile: (cos, sin) of key positions n0 .. n0 + kpw - 1 for pairs
+  // 32p .. 32p + 31, computed from the fp64 positions and frequencies
+  auto load_tab = [&](int p, int buf) {
     for (int v = tid; v < kpw * 16; v += 256) {
       const int pos = v >> 4, j2 = (v & 15) * 2;
       const int n = n0 + pos;
       f32x4 cs = {1.f, 0.f, 1.f, 0.f};
-      if (n < a.N) cs = *(const f32x4*)(a.tab + (long)n * hh + 32 * p + j2);
+      if (n < a.N) {
+        const double pn = a.pos[n];
+        const float2 c0 = rope_cs(pn, a.invf[32 * p + j2]), c1 = rope_cs(pn, a.invf[32 * p + j2 + 1]);
+        cs = f32x4{c0.x, c0.y, c1.x, c1.y};
+      }
       *(f32x4*)&Ts[(buf * kpw + pos) * TS + j2] = cs;
     }
   };

@@ -127,7 +127,8 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
   CT* k = (CT*)(ws + p.k);
   float* partk = (float*)(ws + p.partk);
   float* rk = (float*)(ws + p.rk);
-  const float2* tab_ck = (const float2*)(ws + p.tab_ck);
+  const float2* tab_ck = m.fp32 ? (const float2*)(ws + p.tab_ck) : nullptr;   // bf16 mode: computed in place
+  const double* invf_c = (const double*)(ws + p.invf_c);
   const float2* tab_cq = (const float2*)(ws + p.tab_cq);
   const float2* tab_bk = (const float2*)(ws + p.tab_bk);
   const float2* tab_bq = (const float2*)(ws + p.tab_bq);
@@ -254,7 +255,8 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
         ka.X = (const f16*)X;
         ka.wkt = wkt;
         ka.bias = bw.ca_bk;
-        ka.tab = tab_ck;
+        ka.pos = positions;
+        ka.invf = invf_c;
         ka.k = (f16*)k;
         ka.part = partk;
         ka.H = m.H;
@@ -358,7 +360,8 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
               rk_.K = Kp;
               rk_.V = Vp;
               rk_.tab_b = tab_bk;
-              rk_.tab_c = tab_ck;
+              rk_.pos = positions;
+              rk_.invf_c = invf_c;
               rk_.wkt = (const f16*)(ws + p.wkt);
               rk_.bias = bw.ca_bk;
               rk_.ridx = ridx;

@@ -15,8 +15,10 @@
 // LDS, where they stay for the whole workgroup.  The product is computed
 // transposed, k~^T = W_K x^T (MFMA rows = output widths, columns =
 // candidates): lane l of an accumulator then holds candidate l % 32 and 16
-// widths in runs of 4, so the query and rotation-table values it needs are
-// 16-byte vector loads and the per-row sums reduce inside the lane.  W_K
+// widths in runs of 4, so the query values it needs are
+// 16-byte vector loads (the compactor-RoPE rotation of each candidate's key
+// position is computed in place from the fp64 position and frequencies) and
+// the per-row sums reduce inside the lane.  W_K
 // fragments stream from the fragment-tiled copy (wtile_off) into a ring of
 // registers (the k loop has no barriers); wave w owns, in column tile ct, the
 // pairs 128 ct + 32 w + [0, 32) (both RoPE members, dc/2 apart) for all BM
@@ -30,7 +32,8 @@ struct RefineKArgs {
   const void* K;          // [H][N][d] RoPE'd keys (IT)
   const void* V;          // [H][N][d] values (IT)
   const float2* tab_b;    // [N][d/2] base RoPE (cos, sin) at the key positions
-  const float2* tab_c;    // [N][dc/2] compactor RoPE (cos, sin) at the key positions
+  const double* pos;      // [N] key positions
+  const double* invf_c;   // [dc/2] compactor RoPE frequencies (fp64)
   const f16* wkt;         // W_K fragment-tiled (wtile_off), nc*dc rows x 2d columns
   const void* bias;       // [nc*dc] b_K (TBias) or NULL
   const int* ridx;        // [H*nc][t*R] key of each candidate slot (< 0: empty)
@@ -231,23 +234,23 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
 #pragma unroll
         for (int i = 0; i < TC; ++i) {
           const int2 ri = rinfo[32 * i + l32];
-          const float2* tr = a.tab_c + (long)ri.x * hh + p0;
+          const double pk = a.pos[ri.x];
           const float* qr = qh + (long)ri.y * Ec + p0;
           float dp = 0.f, sp = 0.f;
 #pragma unroll
           for (int jq = 0; jq < 4; ++jq) {
+            // four rotations at a time (keeps the fp64 angle work from being
+            // hoisted all at once, which would cost occupancy)
+            __builtin_amdgcn_sched_barrier(0);
             const f32x4 q0 = *(const f32x4*)(qr + 8 * jq);
             const f32x4 q1 = *(const f32x4*)(qr + 8 * jq + hh);
-            const f32x4 c01 = *(const f32x4*)(tr + 8 * jq);
-            const f32x4 c23 = *(const f32x4*)(tr + 8 * jq + 2);
-            const float cc[4] = {c01[0], c01[2], c23[0], c23[2]};
-            const float ss[4] = {c01[1], c01[3], c23[1], c23[3]};
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
+              const float2 rc = rope_cs(pk, a.invf_c[p0 + 8 * jq + u]);
               const float v0 = acc[i][0][4 * jq + u] + bs0[4 * jq + u];
               const float v1 = acc[i][1][4 * jq + u] + bs1[4 * jq + u];
               sp += v0 * v0 + v1 * v1;
-              const float y0 = v0 * cc[u] - v1 * ss[u], y1 = v1 * cc[u] + v0 * ss[u];
+              const float y0 = v0 * rc.x - v1 * rc.y, y1 = v1 * rc.x + v0 * rc.y;
               dp += y0 * q0[u] + y1 * q1[u];
             }
           }

@@ -68,6 +68,14 @@ def test_config1_variants(variant):
     _case(configs.shrink(W1, **ch), name=f"cfg1 {variant}")
 
 
+@pytest.mark.parametrize("ds,t", [(128, 300), (128, 1024), (128, 1), (256, 257), (384, 300), (512, 100)])
+def test_self_attention_head_widths(ds, t):
+    """Latent self-attention on the cfg-1 cache with self heads d_s wide: the
+    flash kernel (d_s 128, 256, 512; t = 1024 splits the keys four ways) and
+    the separate score / softmax / product passes (d_s 384), ragged t."""
+    _case(configs.shrink(W1, self_head_dim=ds), N=1000, t=t, name=f"cfg1 d_s={ds} t={t}")
+
+
 @pytest.mark.parametrize("mode", [pytest.param(configs.MODE_BF16, marks=MULTI_BLOCK_XFAIL), configs.MODE_FP32])
 def test_config1_two_blocks_gelu_final_norm(mode):
     _case(configs.shrink(W1, n_blocks=2, ffn_kind=configs.FFN_GELU, final_norm=1), mode=mode,
