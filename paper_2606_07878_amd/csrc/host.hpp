@@ -147,12 +147,13 @@ struct Dims {
 };
 
 struct Plan {
-  size_t pq, tab_ck, tab_cq, tab_bk, tab_bq;
+  size_t pq, tab_ck, tab_cq, tab_bq;   // (cos, sin) tables of the latent positions (and, fp32 mode, of the keys)
   size_t wconv;          // bf16 mode: the layer's weight matrices converted to fp16
   size_t wkt;            // bf16 mode: fragment-tiled fp16 copy of the cross-attention W_K
   size_t X, XT, Z, Y, q, partq, rq, O;
   size_t Ylo, qex, cval, cidx, ocnt, ridx, rval, rcnt, rpart, crow, ccount;   // logit refinement
-  size_t q64, invf_b, invf_c;   // fp32 mode: fp64 queries and RoPE frequencies of the refinement
+  size_t q64;                   // fp32 mode: fp64 queries of the refinement
+  size_t invf_b, invf_c;        // fp64 RoPE frequencies (base, compactor)
   size_t kvpart, hscale;        // bf16 mode: per-head fp16 range scale of the staged cache
   // union region: cross-attention key side ...
   size_t k, partk, rk, opart, mpart, lpart;
@@ -314,7 +315,7 @@ inline Plan make_plan(const still_config* c, const Dims& m) {
   p.tab_ck = m.fp32 ? take(8ul * m.N * (m.dc / 2)) : 0;
   p.invf_c = take(8ul * (m.dc / 2));
   p.tab_cq = take(8ul * m.t * (m.dc / 2));
-  p.tab_bk = take(8ul * m.N * (m.d / 2));
+  p.invf_b = take(8ul * (m.d / 2));   // base RoPE frequencies (fp64): staging and refinement rotate in place
   p.tab_bq = take(8ul * m.t * (m.d / 2));
   p.wconv = m.fp32 ? 0 : take(2ul * matrix_elems(c, m));
   p.kvpart = m.fp32 ? 0 : take(4ul * m.H * stage_blocks(m));
@@ -343,7 +344,6 @@ inline Plan make_plan(const still_config* c, const Dims& m) {
     p.rpart = take(8ul * HCT * m.R);
     if (m.fp32) {
       p.q64 = take(8ul * Ht * m.Ec);
-      p.invf_b = take(8ul * (m.d / 2));
     }
     p.crow = take(4ul * HCT * m.R);
     p.ccount = take(4ul * m.H * m.nc);

@@ -130,7 +130,7 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
   const float2* tab_ck = m.fp32 ? (const float2*)(ws + p.tab_ck) : nullptr;   // bf16 mode: computed in place
   const double* invf_c = (const double*)(ws + p.invf_c);
   const float2* tab_cq = (const float2*)(ws + p.tab_cq);
-  const float2* tab_bk = (const float2*)(ws + p.tab_bk);
+  const double* invf_b = (const double*)(ws + p.invf_b);
   const float2* tab_bq = (const float2*)(ws + p.tab_bq);
   const float LOG2E = 1.4426950408889634f;
   // wide GEMM tiles for the paired projections when the head widths allow them
@@ -182,14 +182,14 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
     TIMED(STILL_K_STAGE);
     float* part = sizeof(CT) == 2 ? (float*)(ws + p.kvpart) : nullptr;
     float* hscale = sizeof(CT) == 2 ? (float*)(ws + p.hscale) : nullptr;
-    hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, tab_bk, m.N,
-                       m.d, X, XT, m.Npad, RW, part, (const float*)hscale, 0);
+    hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, positions,
+                       invf_b, m.N, m.d, X, XT, m.Npad, RW, part, (const float*)hscale, 0);
     HIP_TRY(hipGetLastError());
     if (hscale) {
       hipLaunchKernelGGL(kv_scale_kernel, dim3(m.H), dim3(256), 0, st, (const float*)part, (int)grid.x, m.H, hscale);
       HIP_TRY(hipGetLastError());
-      hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, tab_bk,
-                         m.N, m.d, X, XT, m.Npad, RW, (float*)nullptr, (const float*)hscale, 1);
+      hipLaunchKernelGGL((stage_x_kernel<IT, CT>), grid, dim3(256), lds, st, (const IT*)Kp, (const IT*)Vp, positions,
+                         invf_b, m.N, m.d, X, XT, m.Npad, RW, (float*)nullptr, (const float*)hscale, 1);
       HIP_TRY(hipGetLastError());
     }
   }
@@ -359,7 +359,7 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
               RefineKArgs rk_;
               rk_.K = Kp;
               rk_.V = Vp;
-              rk_.tab_b = tab_bk;
+              rk_.invf_b = invf_b;
               rk_.pos = positions;
               rk_.invf_c = invf_c;
               rk_.wkt = (const f16*)(ws + p.wkt);

@@ -137,7 +137,8 @@ static __global__ __launch_bounds__(256) void kv_scale_kernel(const float* __res
 // workgroups of the other heads exit at once).
 template <class IT, class CT>
 __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, const IT* __restrict__ V,
-                                                      const float2* __restrict__ tab, long N, int d,
+                                                      const double* __restrict__ pos, const double* __restrict__ invf,
+                                                      long N, int d,
                                                       CT* __restrict__ X, CT* __restrict__ XT, long ldxt,
                                                       int RW, float* __restrict__ part, const float* __restrict__ hscale,
                                                       int pass) {
@@ -166,15 +167,13 @@ __global__ __launch_bounds__(256) void stage_x_kernel(const IT* __restrict__ K, 
         load8(Kh + n * d + j + hh, b);
 #pragma unroll
         for (int u = 0; u < 8; ++u) amax = fmaxf(amax, fmaxf(fabsf(a[u]), fabsf(b[u])));
-        const f32x4* tp = (const f32x4*)(tab + n * hh + j);
+        const double pn = pos[n];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const f32x4 cs = tp[u];   // (cos, sin) of pairs j+2u, j+2u+1
+        for (int u = 0; u < 8; ++u) {
+          const float2 cs = rope_cs(pn, invf[j + u]);   // base RoPE of pair j + u at position n
           // inverse rotation: (a, b) -> (a cos + b sin, b cos - a sin)
-          y0[2 * u] = a[2 * u] * cs[0] + b[2 * u] * cs[1];
-          y1[2 * u] = b[2 * u] * cs[0] - a[2 * u] * cs[1];
-          y0[2 * u + 1] = a[2 * u + 1] * cs[2] + b[2 * u + 1] * cs[3];
-          y1[2 * u + 1] = b[2 * u + 1] * cs[2] - a[2 * u + 1] * cs[3];
+          y0[u] = a[u] * cs.x + b[u] * cs.y;
+          y1[u] = b[u] * cs.x - a[u] * cs.y;
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) {

@@ -31,8 +31,8 @@ namespace still {
 struct RefineKArgs {
   const void* K;          // [H][N][d] RoPE'd keys (IT)
   const void* V;          // [H][N][d] values (IT)
-  const float2* tab_b;    // [N][d/2] base RoPE (cos, sin) at the key positions
   const double* pos;      // [N] key positions
+  const double* invf_b;   // [d/2] base RoPE frequencies (fp64)
   const double* invf_c;   // [dc/2] compactor RoPE frequencies (fp64)
   const f16* wkt;         // W_K fragment-tiled (wtile_off), nc*dc rows x 2d columns
   const void* bias;       // [nc*dc] b_K (TBias) or NULL
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
       const long n = rinfo[r].x;
       f16* row = As + r * LA;
       float k0[4], k1[4], v0[4], v1[4];
-      f32x4 cs01 = {1.f, 0.f, 1.f, 0.f}, cs23 = {1.f, 0.f, 1.f, 0.f};
+      float cc[4] = {1.f, 1.f, 1.f, 1.f}, ss[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int u = 0; u < 4; ++u) k0[u] = k1[u] = v0[u] = v1[u] = 0.f;
       if (ok) {
@@ -130,11 +130,14 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
         load4f(kr + j + HD, k1);
         load4f(vr + j, v0);
         load4f(vr + j + HD, v1);
-        cs01 = *(const f32x4*)(a.tab_b + n * HD + j);
-        cs23 = *(const f32x4*)(a.tab_b + n * HD + j + 2);
+        const double pn = a.pos[n];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {   // base RoPE of pairs j .. j + 3 at the key's position
+          const float2 cs = rope_cs(pn, a.invf_b[j + u]);
+          cc[u] = cs.x;
+          ss[u] = cs.y;
+        }
       }
-      const float cc[4] = {cs01[0], cs01[2], cs23[0], cs23[2]};
-      const float ss[4] = {cs01[1], cs01[3], cs23[1], cs23[3]};
       half4 h0, h1, l0, l1, w0, w1;
 #pragma unroll
       for (int u = 0; u < 4; ++u) {

@@ -28,13 +28,10 @@ static still_status prepare_tables(const Dims& m, const Plan& p, char* ws, const
                      (double*)(ws + p.invf_c));
   HIP_TRY(hipGetLastError());
   HIP_TRY(table(pq, m.t, m.dc, cbase, p.tab_cq));
-  HIP_TRY(table(positions, m.N, m.d, rope_theta, p.tab_bk));
   if (rerotate) HIP_TRY(table(pq, m.t, m.d, rope_theta, p.tab_bq));
-  if (m.fp32 && m.R > 0) {   // fp64 RoPE frequencies of the fp32 mode's logit refinement
-    hipLaunchKernelGGL(inv_freq64_kernel, dim3((m.d / 2 + 255) / 256), dim3(256), 0, st, rope_theta, m.d,
-                       (double*)(ws + p.invf_b));
-    HIP_TRY(hipGetLastError());
-  }
+  hipLaunchKernelGGL(inv_freq64_kernel, dim3((m.d / 2 + 255) / 256), dim3(256), 0, st, rope_theta, m.d,
+                     (double*)(ws + p.invf_b));
+  HIP_TRY(hipGetLastError());
   return STILL_OK;
 }
 
