@@ -384,28 +384,35 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int NI = NBLK / 4;                  // blocks per wave and stage
   static_assert(NBLK % 4 == 0 && BM % RPB == 0 && ST == 2, "direct load blocks");
   const int w = __builtin_amdgcn_readfirstlane(wave);
-  const int nk = K / BK;
-  const CT* src[NI];
+  // split A (C = (A + A2) B^T): a second pass over K reads the low part
+  const CT* Alo = g.A2 ? (const CT*)g.A2 + b1 * g.sA1 + b2 * g.sA2 : nullptr;
+  const int nk1 = K / BK;
+  const int nk = Alo ? 2 * nk1 : nk1;
+  const CT* src[NI];     // first pass
+  const CT* srclo[NI];   // second pass (A rows from A2; B rows unchanged)
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int rho = (i * 4 + w) * RPB + lane / KV;
     const int u = (lane % KV) ^ lds_swz<KV>(rho);   // rho and rho - BM agree mod 16
     if (rho < BM) {
       const long gr = grow(rho);
-      src[i] = (const CT*)A + (gr >= 0 ? gr * g.lda : 0) + u * E;
+      const long off = (gr >= 0 ? gr * g.lda : 0) + u * E;
+      src[i] = (const CT*)A + off;
+      srclo[i] = Alo ? Alo + off : src[i];
     } else {
       bool valid;
       const TB* bp = b_row(rho - BM, valid);
-      src[i] = (const CT*)(valid ? bp : B) + u * E;
+      src[i] = srclo[i] = (const CT*)(valid ? bp : B) + u * E;
     }
   }
   // k step kn into stage kn % 2
   auto dma = [&](int kn) {
     CT* st = smem_ct + (kn & 1) * SS;
-    const long ks = (long)kn * BK;
+    const bool lo = kn >= nk1;
+    const long ks = (long)(lo ? kn - nk1 : kn) * BK;
 #pragma unroll
     for (int i = 0; i < NI; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(src[i] + ks),
+      __builtin_amdgcn_global_load_lds((const void*)((lo ? srclo[i] : src[i]) + ks),
                                        (__attribute__((address_space(3))) void*)(st + (i * 4 + w) * 512), 16, 0, 0);
   };
   // this wave's loads of all but the newest n k steps have landed and its

@@ -26,11 +26,11 @@ constexpr int GEMM_LONG_K = 512;
 // Direct global -> LDS operand loads (two LDS stages, the next k step's copy
 // in flight during the current one's MFMAs; bit-identical results) apply to fp16
 // operands with whole k steps, 16-byte aligned rows and batch strides and no
-// split or wrapped operand; paired kinds also need whole runs of 8 pairs.
+// wrapped operand; paired kinds also need whole runs of 8 pairs.
 static bool direct_ok(const GemmArgs& g, int bk, bool paired) {
   auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
-  return g.K % bk == 0 && !g.A2 && !g.bwrap && g.lda % 8 == 0 && g.ldb % 8 == 0 && g.sA1 % 8 == 0 &&
-         g.sA2 % 8 == 0 && g.sB1 % 8 == 0 && g.sB2 % 8 == 0 && (g.mgroups <= 1 || g.mgstride % 8 == 0) && al(g.A) &&
+  return g.K % bk == 0 && !g.bwrap && g.lda % 8 == 0 && g.ldb % 8 == 0 && g.sA1 % 8 == 0 && g.sA2 % 8 == 0 &&
+         g.sB1 % 8 == 0 && g.sB2 % 8 == 0 && (g.mgroups <= 1 || g.mgstride % 8 == 0) && al(g.A) && (!g.A2 || al(g.A2)) &&
          al(g.B) && (!g.B2 || al(g.B2)) && (!paired || g.N % 8 == 0);
 }
 
