@@ -120,6 +120,53 @@ def copy_probe(mib: int, dev) -> None:
     del src, dst
 
 
+# MI355X: 8 XCDs (GRBM_GUI_ACTIVE is summed over them), 1024 SIMDs
+N_XCD, N_SIMD = 8, 1024
+
+
+def summarize_counters(path: str, top: int = 40) -> None:
+    """Per-kernel means of a rocprofv3 counter-collection CSV (one row per
+    dispatch and counter), with the derived figures used in the profiles:
+    MFMA busy fraction = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024),
+    f16 MFMA rate = SQ_INSTS_VALU_MFMA_MOPS_F16 x 512 flops per dispatch time,
+    DRAM bytes read = TCC_EA0_RDREQ_DRAM_32B x 32, written = TCC_EA0_WRREQ_DRAM x 64,
+    FETCH_SIZE / WRITE_SIZE in KiB as counted."""
+    import collections
+    import csv
+    import re
+    acc = collections.defaultdict(lambda: collections.defaultdict(float))
+    disp = collections.defaultdict(set)
+    dur = collections.defaultdict(dict)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            name = re.sub(r"\(.*", "", r["Kernel_Name"])[:96] + f" grid={r['Grid_Size']}"
+            disp[name].add(r["Dispatch_Id"])
+            acc[name][r["Counter_Name"]] += float(r["Counter_Value"])
+            dur[name][r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    order = sorted(acc, key=lambda k: -sum(dur[k].values()))[:top]
+    for name in order:
+        n = len(disp[name])
+        m = {c: v / n for c, v in acc[name].items()}
+        us = sum(dur[name].values()) / n / 1e3
+        parts = [f"n={n}", f"avg_us={us:.1f}"]
+        if "GRBM_GUI_ACTIVE" in m and "SQ_VALU_MFMA_BUSY_CYCLES" in m:
+            parts.append(f"mfma_busy={m['SQ_VALU_MFMA_BUSY_CYCLES'] / (m['GRBM_GUI_ACTIVE'] / N_XCD * N_SIMD):.3f}")
+        if "SQ_INSTS_VALU_MFMA_MOPS_F16" in m and us > 0:
+            parts.append(f"f16_TFLOPs={m['SQ_INSTS_VALU_MFMA_MOPS_F16'] * 512 / us * 1e-6:.1f}")
+        if "SQ_LDS_IDX_ACTIVE" in m and "SQ_LDS_BANK_CONFLICT" in m and m["SQ_LDS_IDX_ACTIVE"] > 0:
+            parts.append(f"lds_conflict_frac={m['SQ_LDS_BANK_CONFLICT'] / m['SQ_LDS_IDX_ACTIVE']:.3f}")
+        if "TCC_EA0_RDREQ_DRAM_32B" in m:
+            rd = m["TCC_EA0_RDREQ_DRAM_32B"] * 32
+            parts.append(f"dram_read_MB={rd / 1e6:.1f} ({rd / us * 1e-6:.2f} TB/s)")
+        if "TCC_EA0_WRREQ_DRAM" in m:
+            wr = m["TCC_EA0_WRREQ_DRAM"] * 64
+            parts.append(f"dram_write_MB={wr / 1e6:.1f} ({wr / us * 1e-6:.2f} TB/s)")
+        for c in ("FETCH_SIZE", "WRITE_SIZE"):
+            if c in m:
+                parts.append(f"{c}_KiB={m[c]:.6g}")
+        print(f"{name} | " + " ".join(parts))
+
+
 def consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding, reps: int = 20, suffix: int = 64) -> dict:
     """One decode step of the base model's attention over every layer
     (query_group query heads per KV head, one query each): over the compact
@@ -355,10 +402,15 @@ def main():
                     help="run one plain device copy of this many MiB first (HBM counter calibration)")
     ap.add_argument("--no-consumer", action="store_true",
                     help="skip the decode-attention measurement (shorter profiler runs)")
+    ap.add_argument("--summarize-counters", metavar="CSV",
+                    help="print per-kernel means of a rocprofv3 counter-collection CSV and exit (no GPU use)")
     ap.add_argument("--consumer-only", action="store_true",
                     help="time only the decode attention over the compacted and the full cache (after one "
                          "compaction step) and print that object")
     args = ap.parse_args()
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the compactor forward runs on a "
               "single MI355X in this build.", file=sys.stderr)

@@ -155,16 +155,26 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   const int wm = wave >> 1, wn = wave & 1;
   const int l32 = lane & 31, lg = lane >> 5;
 
-  // Tile order.  Workgroup ids are dealt to the 8 XCDs round robin; XCD x
-  // takes the M tiles congruent to x mod 8 (so that rows cut short by a
-  // device-side row count leave every XCD the same share of work) and walks
+  // Tile order.  Workgroup ids are dealt to the 8 XCDs round robin.  A
+  // batched product with few tiles per batch (and a multiple of 8 batches)
+  // keeps every batch on one XCD, whose L2 then serves all its tiles' operand
+  // reuse.  Otherwise XCD x takes the M tiles congruent to x mod 8 and walks
   // them in groups of 8 M tiles x all N tiles, so that the operand tiles its
   // concurrent workgroups touch stay in its L2.
   const int gx = gridDim.x, gy = gridDim.y;
   int lin = blockIdx.x + gx * blockIdx.y;
+  int bz = blockIdx.z;
   constexpr int GM = 8;
   int mt0, nt;
-  if ((gy & 7) == 0) {
+  if ((gridDim.z & 7) == 0 && gx * gy <= 64) {
+    const int T = gx * gy;
+    const int gid = lin + T * blockIdx.z;            // dispatch order
+    const int xcd = gid & 7, i = gid >> 3;
+    bz = (i / T) * 8 + xcd;
+    lin = i - (i / T) * T;
+    mt0 = lin / gx;
+    nt = lin - mt0 * gx;
+  } else if ((gy & 7) == 0) {
     const int xcd = lin & 7, i = lin >> 3, gyx = gy >> 3;
     const int grp = i / (GM * gx), gm0 = grp * GM;
     const int gsz = min(GM, gyx - gm0);
@@ -181,7 +191,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     nt = inl / gsz;
   }
 
-  const int bz = blockIdx.z, b1 = bz / g.nb2, b2 = bz - b1 * g.nb2;
+  const int b1 = bz / g.nb2, b2 = bz - b1 * g.nb2;
   const int M = g.M;
   {
   const int mt = mt0;
