@@ -228,6 +228,38 @@ def consumer_attend(w, Ck, Cv, Ks, Vs, dev, binding, reps: int = 20, suffix: int
     return res
 
 
+def backward_measure(wid: int, dev, binding, reps: int = 3, N: int = 8192, t: int = 256) -> dict:
+    """One layer of the compactor backward pass (still_compact_layer_backward,
+    fp32 mode: forward with saved activations, then the reverse sweep) at
+    the workload's compactor shape on an N-token cache compacted to t.
+    Algorithmic FLOPs: three times the forward layer's (the forward itself,
+    then one product each for the input and the weight gradients)."""
+    import torch
+    from paper_2606_07878_amd import configs, synth
+    w = configs.shrink(configs.get_workload(wid), n_tokens=N, t=t)
+    K, V, pos, W = synth.make_layer_torch(w, 0, dev, dtype=torch.float32)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(99)
+    dCk = torch.randn(w.cfg.n_kv_heads, t, w.cfg.head_dim, generator=gen, device=dev)
+    dCv = torch.randn(w.cfg.n_kv_heads, t, w.cfg.head_dim, generator=gen, device=dev)
+    ccfg = binding.make_config(w.cfg, configs.MODE_FP32)
+    ws = torch.empty(binding.still_backward_workspace_size(ccfg, N, t), dtype=torch.uint8, device=dev)
+    binding.compact_layer_backward(w.cfg, W, K, V, pos, w.rope_theta, t, dCk, dCv, workspace=ws)   # warm-up
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        binding.compact_layer_backward(w.cfg, W, K, V, pos, w.rope_theta, t, dCk, dCv, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    flops = 3.0 * layer_flops(w, N)
+    return {"workload": f"{w.name}, backward of one layer, N {N} -> t {t}, fp32 mode", "ms_per_layer": round(ms, 3),
+            "reps": reps, "algorithmic_tflop": round(flops * 1e-12, 4),
+            "achieved_tflops": round(flops / (ms * 1e-3) * 1e-12, 2),
+            "frac_of_fp32_mfma_peak": round(flops / (ms * 1e-3) / 157.3e12, 4)}
+
+
 def kv_stream_bytes(w, N=None) -> dict:
     """Bytes of the RoPE-fix staging kernel per layer: the KV cache read once
     (the algorithmic stream) and the fp16 X / X^T copies it writes."""
@@ -400,6 +432,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (HBM counter calibration)")
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward-pass measurement")
     ap.add_argument("--no-consumer", action="store_true",
                     help="skip the decode-attention measurement (shorter profiler runs)")
     ap.add_argument("--summarize-counters", metavar="CSV",
@@ -447,6 +480,9 @@ def main():
     out.update({k: v for k, v in head.items() if k not in ("value", "ms_per_step")})
     if workloads:
         out["workloads"] = workloads
+    if not args.no_backward:
+        print("[bench] timing the backward pass", file=sys.stderr, flush=True)
+        out["backward"] = backward_measure(args.workload, dev, binding)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on bounded samples", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(configs.get_workload(args.workload))

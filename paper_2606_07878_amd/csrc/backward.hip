@@ -26,6 +26,7 @@ struct BPlan {
   size_t Zs[8], Ys[8], rs[8], qst[8], qsn[8], qs[8], kst[8], ksn[8], ks[8], vs[8], Ps[8], Hs[8];
   size_t Zf[8], Yf[8], rf[8], g[8], u[8], a[8];
   size_t Zo, ro, dZ, dY, dH, dP, dq, dk, dv, dA, dU, dck;
+  size_t csp;   // column-sum chunk partials (bias gradients)
   size_t total;
 };
 constexpr int BWD_MAX_BLOCKS = 8;
@@ -97,6 +98,7 @@ BPlan make_bplan(const still_config* c, const Dims& m) {
   p.dA = take(4 * Ht * std::max(m.F, 1));
   p.dU = take(4 * Ht * std::max(m.F, 1));
   p.dck = take(4 * Ht * m.d);
+  p.csp = take(8ul * COLSUM_CHUNKS * std::max(m.Ec, std::max(m.Es, 1)));
   p.total = off + 256;
   return p;
 }
@@ -199,8 +201,13 @@ still_status run_backward(const still_config* cfg, const Dims& m, const BPlan& p
   auto colsum = [&](auto* dx, long rows, long ld, int wd, float* db) -> hipError_t {
     if (!db) return hipSuccess;
     typedef typename std::remove_const<typename std::remove_pointer<decltype(dx)>::type>::type T;
-    hipLaunchKernelGGL((b_colsum_kernel<T>), dim3((unsigned)((wd + 255) / 256)), dim3(256), 0, st, (const T*)dx, rows,
-                       ld, wd, db);
+    double* part = (double*)(ws + p.csp);
+    hipLaunchKernelGGL((b_colsum_part_kernel<T>), dim3((unsigned)((wd + 255) / 256), COLSUM_CHUNKS), dim3(256), 0, st,
+                       (const T*)dx, rows, ld, wd, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(b_colsum_fin_kernel, dim3((unsigned)((wd + 255) / 256)), dim3(256), 0, st, (const double*)part,
+                       COLSUM_CHUNKS, wd, db);
     return hipGetLastError();
   };
   auto W = [](const void* x) { return (const float*)x; };

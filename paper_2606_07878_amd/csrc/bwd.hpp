@@ -119,10 +119,16 @@ __global__ __launch_bounds__(256) void sgemm_kernel(SgemmArgs g) {
   }
 }
 
-// The same product with fp64 accumulation (plain FMAs, 64 x 64 tiles, 4 x 4
-// outputs per thread), for the steps whose rounding the d_l logit scale
-// amplifies: the cross-attention logit path and its adjoint.  Operands and
-// result may be float or double.
+// The same product in fp64 (fp64 MFMA, v_mfma_f64_16x16x4_f64), for the
+// steps whose rounding the d_l logit scale amplifies: the cross-attention
+// logit path and its adjoint.  Operands and result may be float or double.
+// 64 x 64 tiles staged through LDS in k chunks of 16; wave (wm, wn) owns the
+// 32 x 32 quadrant (wm, wn) as 2 x 2 MFMA tiles of 16 x 16.  Operand layout
+// of the MFMA: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16] of
+// the 16 x 4 and 4 x 16 step; the result is C[l / 16 + 4 v][l % 16] in
+// register pair v of lane l (checked with a probe on the hardware).
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
 template <bool AK, bool BK, class TA, class TB, class TC>
 __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __restrict__ A0, const TB* __restrict__ B0,
                                                     TC* __restrict__ C0) {
@@ -134,12 +140,13 @@ __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __res
   const int b = blockIdx.z, b1 = b / g.nb2, b2 = b - b1 * g.nb2;
   const TA* A = A0 + b1 * g.sa1 + b2 * g.sa2;
   const TB* B = B0 + b1 * g.sb1 + b2 * g.sb2;
-  const int tr = tid >> 4, tc = tid & 15;
-  double acc[4][4];
+  const int lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
+  const int li = lane & 15, lk = lane >> 4;
+  f64x4 acc[2][2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+    for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
   for (int k0 = 0; k0 < g.K; k0 += KS) {
     for (int e = tid; e < T * KS; e += 256) {
       // consecutive threads walk the operand's contiguous dimension
@@ -154,33 +161,32 @@ __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __res
     }
     __syncthreads();
 #pragma unroll
-    for (int k = 0; k < KS; ++k) {
-      double av[4], bv[4];
+    for (int k = 0; k < KS; k += 4) {
+      double av[2], bv[2];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = As[k][tr + 16 * i];
+      for (int i = 0; i < 2; ++i) av[i] = As[k + lk][32 * wm + 16 * i + li];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) bv[j] = Bs[k][tc + 16 * j];
+      for (int j = 0; j < 2; ++j) bv[j] = Bs[k + lk][32 * wn + 16 * j + li];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fma(av[i], bv[j], acc[i][j]);
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[i], bv[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
   TC* C = C0 + b1 * g.sc1 + b2 * g.sc2;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + tr + 16 * i;
-    if (m >= g.M) continue;
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int n = n0 + tc + 16 * j;
-      if (n >= g.N) continue;
-      TC* c = C + (long)m * g.ldc + n;
-      const double v = (double)g.alpha * acc[i][j] + (g.bias ? (double)g.bias[n] : 0.0);
-      *c = (TC)(g.accumulate ? (double)*c + v : v);
-    }
-  }
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int m = m0 + 32 * wm + 16 * i + lk + 4 * v, n = n0 + 32 * wn + 16 * j + li;
+        if (m >= g.M || n >= g.N) continue;
+        TC* c = C + (long)m * g.ldc + n;
+        const double val = (double)g.alpha * acc[i][j][v] + (g.bias ? (double)g.bias[n] : 0.0);
+        *c = (TC)(g.accumulate ? (double)*c + val : val);
+      }
 }
 
 // ---------------------------------------------------------------------------
@@ -374,15 +380,27 @@ static __global__ void b_act_bwd_kernel(const float* __restrict__ g, const float
   }
 }
 
-// db[j] = sum over rows of dX[row][j], j < w (ld = row stride), summed in
-// fp64 in row order (deterministic); one thread per column.
+// db[j] = sum over rows of dX[row][j], j < w (ld = row stride), in fp64 and
+// in a fixed order (deterministic): chunk c of gridDim.y sums rows
+// [c R, c R + R) per column into part[c][j] (one thread per column), then the
+// chunks are added in order.
+constexpr int COLSUM_CHUNKS = 64;
 template <class T>
-__global__ __launch_bounds__(256) void b_colsum_kernel(const T* __restrict__ dX, long rows, long ld, int w,
-                                                       float* __restrict__ db) {
+__global__ __launch_bounds__(256) void b_colsum_part_kernel(const T* __restrict__ dX, long rows, long ld, int w,
+                                                            double* __restrict__ part) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= w) return;
+  const long R = (rows + gridDim.y - 1) / gridDim.y;
+  const long r0 = blockIdx.y * R, r1 = r0 + R < rows ? r0 + R : rows;
+  double s = 0.0;
+  for (long r = r0; r < r1; ++r) s += dX[r * ld + j];
+  part[(long)blockIdx.y * w + j] = s;
+}
+static __global__ void b_colsum_fin_kernel(const double* __restrict__ part, int chunks, int w, float* __restrict__ db) {
   const int j = blockIdx.x * 256 + threadIdx.x;
   if (j >= w) return;
   double s = 0.0;
-  for (long r = 0; r < rows; ++r) s += dX[r * ld + j];
+  for (int c = 0; c < chunks; ++c) s += part[(long)c * w + j];
   db[j] = (float)s;
 }
 
