@@ -122,7 +122,7 @@ __global__ __launch_bounds__(256) void sgemm_kernel(SgemmArgs g) {
 // The same product in fp64 (fp64 MFMA, v_mfma_f64_16x16x4_f64), for the
 // steps whose rounding the d_l logit scale amplifies: the cross-attention
 // logit path and its adjoint.  Operands and result may be float or double.
-// 64 x 64 tiles staged through LDS in k chunks of 16; wave (wm, wn) owns the
+// 64 x 64 tiles staged through LDS in k chunks of 32; wave (wm, wn) owns the
 // 32 x 32 quadrant (wm, wn) as 2 x 2 MFMA tiles of 16 x 16.  Operand layout
 // of the MFMA: lane l supplies A[l % 16][l / 16] and B[l / 16][l % 16] of
 // the 16 x 4 and 4 x 16 step; the result is C[l / 16 + 4 v][l % 16] in
@@ -132,7 +132,7 @@ typedef double f64x4 __attribute__((ext_vector_type(4)));
 template <bool AK, bool BK, class TA, class TB, class TC>
 __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __restrict__ A0, const TB* __restrict__ B0,
                                                     TC* __restrict__ C0) {
-  constexpr int T = 64, KS = 16;
+  constexpr int T = 64, KS = 32, PER = T * KS / 256;
   __shared__ double As[KS][T + 1];
   __shared__ double Bs[KS][T + 1];
   const int tid = threadIdx.x;
@@ -147,19 +147,36 @@ __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __res
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
-  for (int k0 = 0; k0 < g.K; k0 += KS) {
-    for (int e = tid; e < T * KS; e += 256) {
-      // consecutive threads walk the operand's contiguous dimension
+  // the next k chunk's operands are loaded into registers while the current
+  // chunk's MFMAs run (consecutive threads walk each operand's contiguous
+  // dimension)
+  double ra[PER], rb[PER];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + 256 * u;
       const int r = AK ? e / KS : e % T, k = AK ? e % KS : e / T;
       const int gr = m0 + r, gk = k0 + k;
-      As[k][r] = (gr < g.M && gk < g.K) ? (double)A[gr * g.am + gk * g.ak] : 0.0;
+      ra[u] = (gr < g.M && gk < g.K) ? (double)A[gr * g.am + gk * g.ak] : 0.0;
     }
-    for (int e = tid; e < T * KS; e += 256) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + 256 * u;
       const int r = BK ? e / KS : e % T, k = BK ? e % KS : e / T;
       const int gr = n0 + r, gk = k0 + k;
-      Bs[k][r] = (gr < g.N && gk < g.K) ? (double)B[gr * g.bn + gk * g.bk] : 0.0;
+      rb[u] = (gr < g.N && gk < g.K) ? (double)B[gr * g.bn + gk * g.bk] : 0.0;
+    }
+  };
+  load(0);
+  for (int k0 = 0; k0 < g.K; k0 += KS) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + 256 * u;
+      As[AK ? e % KS : e / T][AK ? e / KS : e % T] = ra[u];
+      Bs[BK ? e % KS : e / T][BK ? e / KS : e % T] = rb[u];
     }
     __syncthreads();
+    if (k0 + KS < g.K) load(k0 + KS);
 #pragma unroll
     for (int k = 0; k < KS; k += 4) {
       double av[2], bv[2];
