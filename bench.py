@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0
 # from rocprofv3 PMC FETCH_SIZE / WRITE_SIZE passes scaled by what the same
 # counters read for a 1 GiB device copy (factors 2.0 and 1.0).  Valid only for
 # the kernel sources with this digest; any later change reports null.
-MEASURED_TRAFFIC = {"workload": 2, "sources_sha256_16": "9fdcdfa8426bf038", "bytes_per_launch": 5546004021}
+MEASURED_TRAFFIC = {"workload": 2, "sources_sha256_16": "b9ecf7944ce25252", "bytes_per_launch": 5690300679}
 KERNEL_SOURCES = ("paper_2606_07878_amd/csrc/attn.hpp", "paper_2606_07878_amd/csrc/common.hpp")
 
 
@@ -124,7 +124,7 @@ def copy_probe(mib: int, dev) -> None:
 N_XCD, N_SIMD = 8, 1024
 
 
-def summarize_counters(path: str, top: int = 40) -> None:
+def summarize_counters(path: str, top: int = 400) -> None:
     """Per-kernel means of a rocprofv3 counter-collection CSV (one row per
     dispatch and counter), with the derived figures used in the profiles:
     MFMA busy fraction = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024),
