@@ -25,7 +25,8 @@
  *   on the current HIP device), except the arrays of per-layer pointers of
  *   still_compact_model and the `blocks` array of still_layer_weights, which
  *   are HOST arrays holding device pointers.  The library never allocates or
- *   frees memory and keeps no device state between calls.
+ *   frees memory and keeps no device state between calls, except the static
+ *   per-GPU array of still_attend_scratch (see there).
  * - Row-major, densely packed layouts.  Matrices are stored [out][in]
  *   (torch.nn.Linear layout): the paper's x W with W in R^{in x out} is
  *   evaluated as x W^T with the stored [out][in] array.
