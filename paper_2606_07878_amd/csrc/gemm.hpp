@@ -638,8 +638,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
                   t0[w] = from_f32<TC>(s0[u + w]);
                   t1[w] = from_f32<TC>(s1[u + w]);
                 }
-                *(uint4*)(d0 + u) = *(const uint4*)t0;
-                *(uint4*)(d1 + u) = *(const uint4*)t1;
+                __builtin_nontemporal_store(*(const u32x4*)t0, (u32x4*)(d0 + u));
+                __builtin_nontemporal_store(*(const u32x4*)t1, (u32x4*)(d1 + u));
               }
             } else {
               for (int u = 0; u < PV && u < nvalid; ++u) {
@@ -652,8 +652,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
               if (vec_ok && (((uintptr_t)g.C2 & 15) == 0)) {
 #pragma unroll
                 for (int u = 0; u < PV; u += 4) {
-                  *(f32x4*)(e0 + u) = f32x4{v0[u], v0[u + 1], v0[u + 2], v0[u + 3]};
-                  *(f32x4*)(e0 + hh + u) = f32x4{v1[u], v1[u + 1], v1[u + 2], v1[u + 3]};
+                  __builtin_nontemporal_store(f32x4{v0[u], v0[u + 1], v0[u + 2], v0[u + 3]}, (f32x4*)(e0 + u));
+                  __builtin_nontemporal_store(f32x4{v1[u], v1[u + 1], v1[u + 2], v1[u + 3]}, (f32x4*)(e0 + hh + u));
                 }
               } else {
                 for (int u = 0; u < PV && u < nvalid; ++u) {
@@ -743,7 +743,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
             TC tmp[VE];
 #pragma unroll
             for (int u = 0; u < VE; ++u) tmp[u] = from_f32<TC>(src[u]);
-            *(uint4*)dst = *(const uint4*)tmp;
+            __builtin_nontemporal_store(*(const u32x4*)tmp, (u32x4*)dst);
           }
         } else {
           for (int u = 0; u < VE && u < nvalid; ++u) {
