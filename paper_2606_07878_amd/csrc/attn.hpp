@@ -295,9 +295,10 @@ namespace still {
 // QK product (64 keys x TT latents per wave) and output features
 // [w D2 / 4, (w + 1) D2 / 4) in the P.X product.
 //   QK: S^T[key][lat] over the head width, in chunks of QC = 64 (one barrier
-//       per chunk).  Q chunks are staged through LDS (three buffers; each
-//       chunk is loaded one chunk ahead of its store), and each step's Q
-//       fragments are read one step ahead of the MFMAs that use them.  K fragments come
+//       per chunk).  Q chunks are copied straight from global memory into a
+//       ring of four LDS stages (direct loads, issued three chunks ahead of
+//       use), and each step's Q fragments are read one step ahead of the
+//       MFMAs that use them.  K fragments come
 //       from the tiled layout straight into a ring of registers one chunk
 //       deep: the slot used now is reloaded with the same step of the next
 //       chunk (of the next block, in a block's last chunk, so those loads
@@ -308,8 +309,9 @@ namespace still {
 //       over the 4 waves through LDS; P (fp16) to LDS [lat][key].
 //   P.X: O^T[feat][lat] += X^T[feat][key] P^T[key][lat]; X^T fragments from
 //       the tiled layout through a ring of XR key steps, P from LDS.
-// Keys past the range end (only in its last block) are masked by a select:
-// their tiled k slots may hold stale values.  The grid is 1-D, ordered so
+// Keys past the range end (only in its last block) are masked by an additive
+// -inf: their tiled k slots must hold finite values (the launches zero them,
+// zero_ktile_tail_kernel).  The grid is 1-D, ordered so
 // that the t tiles of one (pair, split) are consecutive workgroups of one
 // XCD and read the same keys through its L2.
 // ---------------------------------------------------------------------------
@@ -320,18 +322,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   constexpr int FW = D2 / NW;            // output features per wave
   constexpr int FT = FW / 32;            // feature tiles per wave
   constexpr int QC = 64, NS = QC / 16;   // Q chunk width; k steps per chunk = K ring depth
-  constexpr int LQ = QC + 8;             // Q stage row stride (halfs)
+  constexpr int NQS = 4, QAHEAD = 3;     // Q stages; chunks between a stage's loads and its use
+  constexpr int QI = TT / 8 / NW;        // Q stage loads per wave and chunk (8 rows of 128 bytes each)
   constexpr int LP = KB + 8;             // P row stride (halfs)
-  constexpr int QV = TT * QC / 8 / NT;   // Q stage vectors per thread
   constexpr int NBK = 2 * NW;            // candidate buckets per latent (wave, lane half)
   constexpr int XR = 4;                  // X^T ring depth (key steps of 16)
   constexpr int PS = KB / 16;            // key steps per block in P.X
-  static_assert(FT >= 1 && QV >= 1 && (TT * QC / 8) % NT == 0, "tile sizes");
+  static_assert(FT >= 1 && QI >= 1 && TT % (8 * NW) == 0, "tile sizes");
 
-  __shared__ __attribute__((aligned(16))) f16 Qs[3][TT * LQ];
+  __shared__ __attribute__((aligned(16))) f16 Qs[NQS][TT * QC];   // rows of 8 swizzled 16-byte units
   __shared__ __attribute__((aligned(16))) f16 Ps[TT * LP];
   __shared__ float red_m[TT][NW], red_l[TT][NW];
-  __shared__ __attribute__((aligned(16))) float rks[2][KB];
+  __shared__ __attribute__((aligned(16))) float rks[2][KB];   // key norm factors (0 past the range end)
+  __shared__ __attribute__((aligned(16))) float kbs[2][KB];   // key mask: 0, or -inf past the range end
   __shared__ float qsl[TT];   // qs of each latent row (read in the softmax, not held in registers)
   __shared__ int ovn[TT];     // overflow entries of each latent row
 
@@ -390,22 +393,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       ti[lt][q] = -1;
     }
 
-  // Q chunk staging (rows past t read the last row and are stored as zeros)
-  half8 qreg[QV];
-  auto load_q = [&](int d0) {
+  // Q chunk staging: wave instruction i fills rows [8 b, 8 b + 8) of a stage
+  // (b = i NW + w, 1 KB); lane l writes unit l % 8 of row 8 b + l / 8 and so
+  // reads the global unit that the swizzle puts there.  Rows past t read the
+  // last row: their logits are finite and never reach a stored output.
+  // The loads are issued from inline assembly: the compiler, seeing direct
+  // loads among the register loads of the K ring, would wait for all of them
+  // before each use of a K fragment.  It still counts the K-ring loads, and
+  // so over-waits by at most the stage loads issued after them; the waits
+  // for the stages are explicit (chunk_barrier).
+  unsigned qoff[QI];
 #pragma unroll
-    for (int i = 0; i < QV; ++i) {
-      const int v = tid + i * NT, r = v / (QC / 8), kk = (v % (QC / 8)) * 8;
-      const unsigned lat = (unsigned)min(t0 + r, a.t - 1);
-      qreg[i] = *(const half8*)(qb + (lat * (unsigned)a.ldq + (unsigned)(d0 + kk)));
+  for (int i = 0; i < QI; ++i) {
+    const int r = 8 * (i * NW + w) + (lane >> 3);
+    const unsigned lat = (unsigned)min(t0 + r, a.t - 1);
+    qoff[i] = lat * (unsigned)a.ldq + 8u * (unsigned)((lane & 7) ^ lds_swz<8>(r));
+  }
+  auto dma_q = [&](int stage, int d0) {
+#pragma unroll
+    for (int i = 0; i < QI; ++i) {
+      const unsigned m0v = (unsigned)(size_t)(__attribute__((address_space(3))) f16*)&Qs[stage][(i * NW + w) * 512];
+      asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                   :: "v"(qb + (qoff[i] + (unsigned)d0)), "s"(m0v) : "memory", "m0");
     }
   };
-  auto store_q = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < QV; ++i) {
-      const int v = tid + i * NT, r = v / (QC / 8), kk = (v % (QC / 8)) * 8;
-      *(half8*)&Qs[buf][r * LQ + kk] = (t0 + r < a.t) ? qreg[i] : zero_frag<f16>();
-    }
+  // Q fragment of latent tile lt, 16-column step js, from a stage
+  auto q_frag = [&](int stage, int lt, int js) -> half8 {
+    const int r = 32 * lt + l32;
+    return *(const half8*)&Qs[stage][r * QC + 8 * ((2 * js + lg) ^ lds_swz<8>(r))];
+  };
+  // Chunks are numbered across blocks (g): chunk g uses stage g % NQS and Q
+  // columns [(g % nch) QC, +QC); it issues the loads of chunk g + QAHEAD into
+  // the stage that chunk g - 1 released, and its last step reads the first
+  // fragments of chunk g + 1.  So at the barrier that ends chunk g the loads
+  // of chunk g + 2 must have landed: they were issued at the start of chunk
+  // g - 1, followed by the K-ring loads of chunk g - 1 and the stage and
+  // K-ring loads of chunk g (more at block boundaries); loads return in
+  // order.  The asm statements also keep the compiler from moving memory
+  // accesses across the barriers.
+  static_assert(NQS == 4 && QAHEAD == 3, "the stage ring and the wait count go together");
+  constexpr int QWAIT = NS * KT + QI + NS * KT;
+  static_assert(QWAIT <= 63, "vmcnt range");
+  auto chunk_barrier = [&]() {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" :: "n"(QWAIT) : "memory");
+  };
+  // this wave's LDS traffic has completed, then all waves meet (stage loads
+  // may still be in flight)
+  auto lds_barrier = [&]() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   };
   // K fragment of this wave's key tile kt of the block at n0, width step js
   auto load_k = [&](int n0, int kt, int js) -> half8 {
@@ -427,25 +462,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   half8 kr[NS][KT];
   half8 xr[XR][FT];
   half8 qf[2][LT];
-  // Q chunks rotate through 3 LDS buffers: the chunk in use (qb0), the next
-  // one (qb1, already visible, so the first fragments of the next chunk can be
-  // read before the chunk boundary) and the one being staged (qb2, Q chunk
-  // qn2 of the head width, loaded one chunk ahead of its store).
-  int qb0 = 0, qb1 = 1, qb2 = 2, qn2 = 2 % nch;
+  int g = 0, qn = QAHEAD % nch;   // chunk number; Q chunk of chunk g + QAHEAD
   int rbuf = 0;
-  // prologue: Q chunks 0 and 1, key norms and K ring of the first block
-  load_q(0);
-  store_q(0);
-  load_q(QC);
-  store_q(1);
+  // prologue: Q chunks 0 .. QAHEAD-1, key norms and K ring of the first block
+#pragma unroll
+  for (int c = 0; c < QAHEAD; ++c) dma_q(c, (c % nch) * QC);
 #pragma unroll
   for (int j = 0; j < NS; ++j)
 #pragma unroll
     for (int kt = 0; kt < KT; ++kt) kr[j][kt] = load_k(nbeg, kt, j);
   rks[0][tid] = load_rk(nbeg);
-  __syncthreads();
+  kbs[0][tid] = nbeg + tid < nend ? 0.f : -INFINITY;
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 #pragma unroll
-  for (int lt = 0; lt < LT; ++lt) qf[0][lt] = *(const half8*)&Qs[0][(32 * lt + l32) * LQ + 8 * lg];
+  for (int lt = 0; lt < LT; ++lt) qf[0][lt] = q_frag(0, lt, 0);
 
   for (int n0 = nbeg; n0 < nend; n0 += KB) {
     const bool next_block = n0 + KB < nend;   // uniform
@@ -463,16 +493,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // first ones in the last step) before its own MFMAs; scheduling barriers
     // keep that order and spread the loads over the chunk.
     auto qk_chunk = [&](int kn0, int ks0) {
-      load_q(qn2 * QC);
-      const f16* Qc = Qs[qb0];
-      const f16* Qn = Qs[qb1];
+      dma_q((g + QAHEAD) & (NQS - 1), qn * QC);
+      const int sc = g & (NQS - 1), sn = (g + 1) & (NQS - 1);
 #pragma unroll
       for (int j = 0; j < NS; ++j) {
-        const f16* src = (j + 1 < NS) ? Qc : Qn;
-        const int col = (j + 1 < NS) ? 16 * (j + 1) : 0;
 #pragma unroll
-        for (int lt = 0; lt < LT; ++lt)
-          qf[(j + 1) & 1][lt] = *(const half8*)&src[(32 * lt + l32) * LQ + col + 8 * lg];
+        for (int lt = 0; lt < LT; ++lt) qf[(j + 1) & 1][lt] = q_frag(j + 1 < NS ? sc : sn, lt, j + 1 < NS ? j + 1 : 0);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int lt = 0; lt < LT; ++lt)
@@ -483,23 +509,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int kt = 0; kt < KT; ++kt) kr[j][kt] = load_k(kn0, kt, ks0 + j);
         __builtin_amdgcn_sched_barrier(0);
       }
-      store_q(qb2);
-      const int t = qb0;
-      qb0 = qb1;
-      qb1 = qb2;
-      qb2 = t;
-      qn2 = qn2 + 1 == nch ? 0 : qn2 + 1;
+      ++g;
+      qn = qn + 1 == nch ? 0 : qn + 1;
     };
     for (int ch = 0; ch + 1 < nch; ++ch) {
       qk_chunk(n0, (ch + 1) * NS);
-      __syncthreads();
+      chunk_barrier();
     }
-    {  // last chunk: the next stage is chunk 0 of the next block (of this block
-       // again at the very end: loaded, never used), with its key norms
-      const float rk_next = load_rk(n0 + KB);
+    {  // last chunk: the K ring moves on to chunk 0 of the next block (of this
+       // block again at the very end: loaded, never used), with its key norms
+      // (the key norm is selected after the chunk: an earlier use would wait
+      // for its load in front of the chunk's stage loads)
+      const int nn = n0 + KB + tid;
+      const float rk_raw = rkb[(long)min(nn, nend - 1) * a.nc];
       qk_chunk(next_block ? n0 + KB : n0, 0);
-      rks[rbuf ^ 1][tid] = rk_next;
-      __syncthreads();
+      rks[rbuf ^ 1][tid] = nn < nend ? rk_raw : 0.f;
+      kbs[rbuf ^ 1][tid] = nn < nend ? 0.f : -INFINITY;
+      chunk_barrier();
     }
     // X^T ring for the block's P.X (arrives during the softmax)
 #pragma unroll
@@ -507,12 +533,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
       for (int f = 0; f < FT; ++f) xr[i][f] = load_x(f, (n0 >> 4) + i);
 
-    // ---- softmax: x = S * rk, masked past the range end, written back over
-    // S; logit (log2 units) = x * qs[lt] (qs > 0, so block maxima of x scale
-    // to those of the logits); one pass for the block maxima, one for the
-    // probabilities
+    // ---- softmax: x = S * rk + kb, written back over S: kb = -inf masks the
+    // keys past the range end without a select (their tiled k slots are zero,
+    // so S is finite there), and fma with a zero addend is exactly the
+    // product; logit (log2 units) = x * qs[lt] (qs > 0, so block maxima of x
+    // scale to those of the logits); one pass for the block maxima, one for
+    // the probabilities
     const float* rkc = rks[rbuf];
-    const bool tail = n0 + KB > nend;
+    const float* kbc = kbs[rbuf];
     float mx[LT], lmx[LT], qs[LT];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) qs[lt] = qsl[32 * lt + l32];
@@ -524,13 +552,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       for (int jq = 0; jq < 4; ++jq) {
         const int kl = KW * w + 32 * kt + 8 * jq + 4 * lg;   // keys of j = 4 jq + u: kl + u
         const float4 r4 = *(const float4*)&rkc[kl];
+        const float4 b4 = *(const float4*)&kbc[kl];
         const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
+        const float kb[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
         for (int lt = 0; lt < LT; ++lt)
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            float x = s[lt][kt][4 * jq + u] * rk[u];
-            if (tail) x = (n0 + kl + u < nend) ? x : -INFINITY;
+            const float x = fmaf(s[lt][kt][4 * jq + u], rk[u], kb[u]);
             s[lt][kt][4 * jq + u] = x;
             mx[lt] = fmaxf(mx[lt], x);
           }
@@ -541,7 +570,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       mx[lt] = fmaxf(mx[lt], __shfl_xor(mx[lt], 32));
       if (lg == 0) red_m[32 * lt + l32][w] = mx[lt] * qs[lt];
     }
-    __syncthreads();
+    lds_barrier();
     float alpha[LT];
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
@@ -634,7 +663,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       }
       m_run[lt] = m_new;
     }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int lt = 0; lt < LT; ++lt) {
       const int li = 32 * lt + l32;
@@ -684,6 +713,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
       __builtin_amdgcn_sched_barrier(0);
     }
   }
+
+  // stage loads of chunks past the end may still be in flight: they land
+  // before the workgroup's LDS is released
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
   // ---- partial (O un-normalised, m, l) of this key range
 #pragma unroll

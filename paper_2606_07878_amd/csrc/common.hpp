@@ -172,4 +172,12 @@ __device__ __forceinline__ f32x16 zero16() {
   return z;
 }
 
+// Swizzle of the 16-byte unit index within an LDS row of U units.  Rows are
+// read 16 at a time at one unit (MFMA fragments) and written U units at a
+// time per row (staging); the mask is a bijection on the row bits that decide
+// the bank group under both 128-byte and 256-byte LDS access phases.
+template <int U> __device__ __forceinline__ int lds_swz(int r);
+template <> __device__ __forceinline__ int lds_swz<4>(int r) { return (((r >> 1) ^ (r >> 3)) & 1) | ((r >> 1) & 2); }
+template <> __device__ __forceinline__ int lds_swz<8>(int r) { return ((r ^ (r >> 3)) & 1) | (r & 6); }
+
 }  // namespace still

@@ -106,14 +106,6 @@ __device__ __forceinline__ void wave_lds_fence() {
   __builtin_amdgcn_wave_barrier();
 }
 
-// Swizzle of the 16-byte unit index within an LDS row of U units.  Rows are
-// read 16 at a time at one unit (MFMA fragments) and written U units at a
-// time per row (staging); the mask is a bijection on the row bits that decide
-// the bank group under both 128-byte and 256-byte LDS access phases.
-template <int U> __device__ __forceinline__ int lds_swz(int r);
-template <> __device__ __forceinline__ int lds_swz<4>(int r) { return (((r >> 1) ^ (r >> 3)) & 1) | ((r >> 1) & 2); }
-template <> __device__ __forceinline__ int lds_swz<8>(int r) { return ((r ^ (r >> 3)) & 1) | (r & 6); }
-
 // LDS arena: two operand stages, reused after the k loop for the epilogue
 // staging (4 waves x 32 rows x (BN/2 + 8) floats).
 template <int BM, int BN, int BK, class CT>

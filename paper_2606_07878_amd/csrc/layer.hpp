@@ -283,6 +283,11 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
           else hipLaunchKernelGGL((kproj_kernel<256, 128, IT>), grid, dim3(256), 0, st, ka);
         }
         HIP_TRY(hipGetLastError());
+        if (m.Npad > m.N) {   // keys past N: finite (zero) slots for the additive mask of the attention
+          hipLaunchKernelGGL(zero_ktile_tail_kernel, dim3(grid1d((long)m.H * m.nc * (m.Npad - m.N) * (m.dc / 8))),
+                             dim3(256), 0, st, (f16*)k, (long)m.H * m.nc, (int)m.N, (long)m.Npad, m.dc);
+          HIP_TRY(hipGetLastError());
+        }
         HIP_TRY(finalize(partk, HN, m.nc, 1, rk));
       } else {  // k = RoPE_c(k~) with k~ = X W_K^T + b_K
         GemmArgs g = gargs((int)HN, m.Ec / 2, m.d2, X, m.d2, bw.ca_wk, m.d2, k, m.Ec);
@@ -508,6 +513,12 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
           g.ctile_npad = m.tpadk;
           if (wide_s) HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR, true>(g, 1, st)));
           else HIP_TRY((gemm<CT, CT, CT, CT, IT, EPI_PAIR>(g, 1, st)));
+          if (m.tpadk > m.t) {   // keys past t: finite (zero) slots for the additive mask of the attention
+            TIMED(STILL_K_OTHER);
+            hipLaunchKernelGGL(zero_ktile_tail_kernel, dim3(grid1d((long)m.H * m.ns * (m.tpadk - m.t) * (m.ds / 8))),
+                               dim3(256), 0, st, (f16*)ks, (long)m.H * m.ns, m.t, (long)m.tpadk, m.ds);
+            HIP_TRY(hipGetLastError());
+          }
         }
         {  // v^T[h] = W_V^sa Y[h]^T, tiled [h][feature tiles][key steps]
           GemmArgs g = gargs(m.Es, m.t, m.D, bw.sa_wv, m.D, Y, m.D, vT, m.tpadk);

@@ -713,6 +713,20 @@ static __global__ void zero_xtile_tail_kernel(f16* __restrict__ A, long rows, in
   }
 }
 
+// Zero keys [n0, npad) of the fragment-tiled key layout (ktile_off) of
+// `heads` heads of width dc, one 16-byte unit per thread and step: the
+// cross-attention masks those keys additively, which needs finite logits.
+static __global__ void zero_ktile_tail_kernel(f16* __restrict__ k, long heads, int n0, long npad, int dc) {
+  const long w = npad - n0, units_per_key = dc / 8;
+  const long total = heads * w * units_per_key;
+  const uint4 z = {0u, 0u, 0u, 0u};
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    const long hc = i / (w * units_per_key), r = i - hc * (w * units_per_key);
+    const long n = n0 + r / units_per_key, x = (r % units_per_key) * 8;
+    *(uint4*)(k + ktile_off(hc, n, x, npad, dc)) = z;
+  }
+}
+
 // Element-type conversion of up to CONV_SEGS weight matrices per launch
 // (bf16 -> fp16 for the MFMA operands), one segment per grid row, 8 elements
 // per thread and step; segment lengths are multiples of 8 and 16-byte aligned.

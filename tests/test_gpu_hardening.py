@@ -12,6 +12,9 @@
   (App. A canonical configuration: d_l = 256, B = 2, n_c = n_s = 1, no FFN).
 * The App. C identity-style initialisation at t = N on the GPU: the compact
   cache reproduces the input cache.
+* A workspace filled with NaN bit patterns before the call, at ragged N and t
+  (key tiles past N and past t are padding): nothing stale may reach the
+  outputs.
 """
 import math
 
@@ -235,3 +238,27 @@ def test_large_cache_magnitudes(wid, outlier, vscale, N, t):
         got = run_gpu(w.cfg, cache, wts, w.rope_theta, t, mode=mode)
         assert_parity((got[0][heads], got[1][heads], got[2]), ref, tol,
                       what=f"large magnitudes cfg{wid} K x{outlier:g} V x{vscale:g} mode{mode}")
+
+
+@pytest.mark.parametrize("mode,tol", MODES)
+def test_poisoned_workspace_ragged_shapes(mode, tol):
+    """cfg-1 compactor (flash self-attention, d_s = 128) at N = 1000, t = 300:
+    the cross-attention's last key tile and the self-attention's last latent
+    tile are partly padding; the workspace starts as all-ones bytes (NaN in
+    fp16 and fp32)."""
+    import torch
+    from paper_2606_07878_amd import binding
+    N, t = 1000, 300
+    cache = synth.make_cache(W1, 0, n_tokens=N)
+    wts = synth.make_weights(W1, 0, t=t)
+    need = binding.still_workspace_size(binding.make_config(W1.cfg, mode), N, t, 1)
+    ws = torch.full((need,), 255, dtype=torch.uint8, device="cuda")
+    K = dev_tensor(cache["K"], mode)
+    V = dev_tensor(cache["V"], mode)
+    pos = torch.from_numpy(cache["positions"]).cuda()
+    W = {k: dev_tensor(v, mode) for k, v in wts.items()}
+    Ck, Cv, p = binding.compact_layer(W1.cfg, W, K, V, pos, W1.rope_theta, t, mode=mode, workspace=ws)
+    torch.cuda.synchronize()
+    got = (Ck.double().cpu().numpy(), Cv.double().cpu().numpy(), p.cpu().numpy())
+    ref = run_oracle(W1.cfg, cache, wts, W1.rope_theta, t)
+    assert_parity(got, ref, tol, what=f"cfg1 N={N} t={t} poisoned workspace mode{mode}")
