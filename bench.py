@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0
 # from rocprofv3 PMC FETCH_SIZE / WRITE_SIZE passes scaled by what the same
 # counters read for a 1 GiB device copy (factors 2.0 and 1.0).  Valid only for
 # the kernel sources with this digest; any later change reports null.
-MEASURED_TRAFFIC = {"workload": 2, "sources_sha256_16": "b9ecf7944ce25252", "bytes_per_launch": 5690300679}
+MEASURED_TRAFFIC = {"workload": 2, "sources_sha256_16": "45660667fe8fff99", "bytes_per_launch": 5558877658}
 KERNEL_SOURCES = ("paper_2606_07878_amd/csrc/attn.hpp", "paper_2606_07878_amd/csrc/common.hpp")
 
 
@@ -419,6 +419,49 @@ def run_workload(wid: int, steps: int, warmup: int, dev, binding, consumer: bool
     return res
 
 
+def library_gemm_reference(wid: int, dev, reps: int = 20) -> dict:
+    """The vendor library's fp16 product (torch.bmm, C = A B with B given as
+    the transpose of a row-major [N][K] operand, fp32 accumulation) timed on
+    the latent-side product shapes of one workload: the practical MFMA rate of
+    the chip on those shapes, for comparison with this library's kernels."""
+    import torch
+    from paper_2606_07878_amd import configs
+    w = configs.get_workload(wid)
+    c = w.cfg
+    H, t = c.n_kv_heads, w.t
+    shapes = {   # name: (batch, M, N, K)
+        "self q/k/v projection": (1, H * t, c.n_self_heads * c.ds, c.latent_dim),
+        "cross q projection": (1, H * t, c.n_cross_heads * c.dc, c.latent_dim),
+        "cross output W_O": (1, H * t, c.latent_dim, c.n_cross_heads * c.dc),
+        "FFN gate+up": (1, H * t, 2 * c.ffn_hidden, c.latent_dim),
+        "FFN down": (1, H * t, c.latent_dim, c.ffn_hidden),
+        "self logits (per head)": (H * c.n_self_heads, t, t, c.ds),
+        "self P v (per head)": (H * c.n_self_heads, t, c.ds, t),
+        "(P X) W_V": (1, H * c.n_cross_heads * t, c.dc, 2 * c.head_dim),
+    }
+    out = {}
+    for name, (b, M, N, K) in shapes.items():
+        a = torch.randn(b, M, K, device=dev, dtype=torch.float16)
+        bt = torch.randn(b, N, K, device=dev, dtype=torch.float16).transpose(1, 2).contiguous()
+        for _ in range(3):
+            torch.bmm(a, bt)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.bmm(a, bt)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / reps * 1e3
+        fl = 2.0 * b * M * N * K
+        out[name] = {"batch": b, "M": M, "N": N, "K": K, "us": round(us, 1), "tflops": round(fl / us * 1e-6, 1),
+                     "frac_of_2.5PF": round(fl / us * 1e-6 / 2500.0, 3)}
+        print(f"[gemm-ref] {name:24s} {b}x{M}x{N}x{K}: {us:8.1f} us {fl / us * 1e-6:7.1f} TFLOP/s", flush=True)
+        del a, bt
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -437,6 +480,9 @@ def main():
                     help="skip the decode-attention measurement (shorter profiler runs)")
     ap.add_argument("--summarize-counters", metavar="CSV",
                     help="print per-kernel means of a rocprofv3 counter-collection CSV and exit (no GPU use)")
+    ap.add_argument("--library-gemm-reference", action="store_true",
+                    help="time the vendor library's fp16 product (torch.bmm) on the latent-side product shapes "
+                         "of --workload and print that object (reference for the MFMA rate, no compaction)")
     ap.add_argument("--consumer-only", action="store_true",
                     help="time only the decode attention over the compacted and the full cache (after one "
                          "compaction step) and print that object")
@@ -456,6 +502,11 @@ def main():
     torch.cuda.set_device(dev)
     if args.copy_probe_mib:
         copy_probe(args.copy_probe_mib, dev)
+    if args.library_gemm_reference:
+        w = configs.get_workload(args.workload)
+        print(json.dumps({"library_gemm_reference": library_gemm_reference(args.workload, dev),
+                          "config": {"workload": w.name}}), flush=True)
+        return
     if args.consumer_only:
         w = configs.get_workload(args.workload)
         res = run_workload(args.workload, 1, args.warmup, dev, binding, consumer=True)
