@@ -20,6 +20,12 @@ namespace still {
 
 namespace {
 
+// Split-K partial buffer of the backward's long-contraction products: its
+// capacity in elements (fp64: 64 MiB) and the current call's buffer (per
+// host thread, set for the duration of run_backward).
+constexpr long KSPLIT_CAP = 8l << 20;
+static thread_local void* t_kpart = nullptr;
+
 struct BPlan {
   size_t pq, invf_b, invf_c, X, Z;
   size_t Zc[8], Yc[8], rc[8], qt[8], qn[8], q[8], kt[8], kn[8], k[8], v[8], P[8], Hc[8];
@@ -27,6 +33,7 @@ struct BPlan {
   size_t Zf[8], Yf[8], rf[8], g[8], u[8], a[8];
   size_t Zo, ro, dZ, dY, dH, dP, dq, dk, dv, dA, dU, dck;
   size_t csp;   // column-sum chunk partials (bias gradients)
+  size_t kpart; // split-K partial sums of the long-contraction products
   size_t total;
 };
 constexpr int BWD_MAX_BLOCKS = 8;
@@ -99,6 +106,7 @@ BPlan make_bplan(const still_config* c, const Dims& m) {
   p.dU = take(4 * Ht * std::max(m.F, 1));
   p.dck = take(4 * Ht * m.d);
   p.csp = take(8ul * COLSUM_CHUNKS * std::max(m.Ec, std::max(m.Es, 1)));
+  p.kpart = take(8ul * KSPLIT_CAP);
   p.total = off + 256;
   return p;
 }
@@ -141,20 +149,50 @@ SgemmArgs gemm_args(int M, int N, int K, Op A, Op B, void* C, long ldc, bool acc
   g.nb2 = bt.nb2;
   g.alpha = alpha;
   g.accumulate = acc ? 1 : 0;
+  g.ksplit = 0;
+  g.part = nullptr;
   g.bias = bias;
   return g;
+}
+
+// Split-K for products with few output tiles and a long contraction (the
+// weight gradients contract over all H N keys or H t latents): grid row z of
+// a one-batch launch takes k in [z kc, (z + 1) kc) and stores raw partial
+// sums in the call's split buffer (set by run_backward for its thread), which
+// ksplit_reduce_kernel sums in order.  Returns the split count (1 = none).
+inline int ksplit_count(int M, int N, int K, long batch) {
+  if (!t_kpart || batch != 1 || K < 2048) return 1;
+  const long tiles = (long)((M + 63) / 64) * ((N + 63) / 64);
+  if (tiles >= 1024) return 1;
+  long s = 2048 / tiles;
+  s = std::min(s, (long)K / 1024);
+  s = std::min(s, 16l);
+  s = std::min(s, KSPLIT_CAP / ((long)M * N));
+  return s >= 2 ? (int)s : 1;
 }
 
 // C = A B^T on the fp32 MFMA kernel (float operands and result)
 hipError_t sgemm(hipStream_t st, int M, int N, int K, Op A, Op B, float* C, long ldc, bool acc,
                  const float* bias = nullptr, Batch bt = Batch(), float alpha = 1.f) {
-  const SgemmArgs g = gemm_args(M, N, K, A, B, C, ldc, acc, bias, bt, alpha);
-  const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64), (unsigned)(bt.nb1 * bt.nb2));
+  SgemmArgs g = gemm_args(M, N, K, A, B, C, ldc, acc, bias, bt, alpha);
+  const int splits = ksplit_count(M, N, K, (long)bt.nb1 * bt.nb2);
+  if (splits > 1) {
+    g.ksplit = (int)((((long)K + splits - 1) / splits + 15) / 16 * 16);
+    g.part = t_kpart;
+  }
+  const int nz = splits > 1 ? (int)(((long)K + g.ksplit - 1) / g.ksplit) : bt.nb1 * bt.nb2;
+  const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64), (unsigned)nz);
   const bool ak = A.ks == 1, bk = B.ks == 1;
   if (ak && bk) hipLaunchKernelGGL((sgemm_kernel<true, true>), grid, dim3(256), 0, st, g);
   else if (ak) hipLaunchKernelGGL((sgemm_kernel<true, false>), grid, dim3(256), 0, st, g);
   else if (bk) hipLaunchKernelGGL((sgemm_kernel<false, true>), grid, dim3(256), 0, st, g);
   else hipLaunchKernelGGL((sgemm_kernel<false, false>), grid, dim3(256), 0, st, g);
+  if (splits > 1) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((ksplit_reduce_kernel<float, float>), dim3(grid1d((long)M * N)), dim3(256), 0, st,
+                       (const float*)t_kpart, nz, M, N, (float*)C, ldc, (double)alpha, bias, acc ? 1 : 0);
+  }
   return hipGetLastError();
 }
 
@@ -162,8 +200,14 @@ hipError_t sgemm(hipStream_t st, int M, int N, int K, Op A, Op B, float* C, long
 template <class TA, class TB, class TC>
 hipError_t dgemm(hipStream_t st, int M, int N, int K, Op A, Op B, TC* C, long ldc, bool acc,
                  const float* bias = nullptr, Batch bt = Batch()) {
-  const SgemmArgs g = gemm_args(M, N, K, A, B, C, ldc, acc, bias, bt, 1.f);
-  const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64), (unsigned)(bt.nb1 * bt.nb2));
+  SgemmArgs g = gemm_args(M, N, K, A, B, C, ldc, acc, bias, bt, 1.f);
+  const int splits = ksplit_count(M, N, K, (long)bt.nb1 * bt.nb2);
+  if (splits > 1) {
+    g.ksplit = (int)((((long)K + splits - 1) / splits + 31) / 32 * 32);
+    g.part = t_kpart;
+  }
+  const int nz = splits > 1 ? (int)(((long)K + g.ksplit - 1) / g.ksplit) : bt.nb1 * bt.nb2;
+  const dim3 grid((unsigned)((N + 63) / 64), (unsigned)((M + 63) / 64), (unsigned)nz);
   const TA* a = (const TA*)A.p;
   const TB* b = (const TB*)B.p;
   const bool ak = A.ks == 1, bk = B.ks == 1;
@@ -171,6 +215,12 @@ hipError_t dgemm(hipStream_t st, int M, int N, int K, Op A, Op B, TC* C, long ld
   else if (ak) hipLaunchKernelGGL((dgemm_kernel<true, false, TA, TB, TC>), grid, dim3(256), 0, st, g, a, b, C);
   else if (bk) hipLaunchKernelGGL((dgemm_kernel<false, true, TA, TB, TC>), grid, dim3(256), 0, st, g, a, b, C);
   else hipLaunchKernelGGL((dgemm_kernel<false, false, TA, TB, TC>), grid, dim3(256), 0, st, g, a, b, C);
+  if (splits > 1) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((ksplit_reduce_kernel<double, TC>), dim3(grid1d((long)M * N)), dim3(256), 0, st,
+                       (const double*)t_kpart, nz, M, N, C, ldc, 1.0, bias, acc ? 1 : 0);
+  }
   return hipGetLastError();
 }
 
@@ -184,6 +234,10 @@ still_status run_backward(const still_config* cfg, const Dims& m, const BPlan& p
   const int H = m.H, t = m.t, nc = m.nc, dc = m.dc, ns = m.ns, ds = m.ds, D = m.D, d = m.d, d2 = m.d2;
   const long Ec = m.Ec, Es = m.Es, F = m.F;
   const long N = m.N;
+  struct KpartScope {   // the split buffer of this call, cleared on every return path
+    explicit KpartScope(void* p) { t_kpart = p; }
+    ~KpartScope() { t_kpart = nullptr; }
+  } kpart_scope(ws + p.kpart);
   auto F32 = [&](size_t off) { return (float*)(ws + off); };
   auto F64 = [&](size_t off) { return (double*)(ws + off); };
   const double* pq = (const double*)(ws + p.pq);

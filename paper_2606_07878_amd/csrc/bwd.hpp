@@ -30,6 +30,12 @@ struct SgemmArgs {
   float alpha;
   int accumulate;
   const float* bias;   // per output column n, added to alpha * acc (NULL = none)
+  // split-K (one batch only): ksplit > 0 makes grid row z sum k in
+  // [z ksplit, (z + 1) ksplit) and store its raw sums (no alpha, bias or
+  // accumulate) into part[z][m][n] (float for the fp32 kernel, double for the
+  // fp64 one); ksplit_reduce_kernel then forms C in a fixed order
+  int ksplit;
+  void* part;
 };
 
 // Stage a 64 x 16 tile (rows r0.., k k0..) of a strided operand into LDS
@@ -90,13 +96,15 @@ __global__ __launch_bounds__(256) void sgemm_kernel(SgemmArgs g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, l32 = lane & 31, lg = lane >> 5;
   const int m0 = blockIdx.y * T, n0 = blockIdx.x * T;
-  const int b = blockIdx.z, b1 = b / g.nb2, b2 = b - b1 * g.nb2;
+  const int kz = g.ksplit ? (int)blockIdx.z : 0;
+  const int b = g.ksplit ? 0 : (int)blockIdx.z, b1 = b / g.nb2, b2 = b - b1 * g.nb2;
+  const int kbeg = kz * g.ksplit, kend = g.ksplit ? min(g.K, kbeg + g.ksplit) : g.K;
   const float* A = g.A + b1 * g.sa1 + b2 * g.sa2;
   const float* B = g.B + b1 * g.sb1 + b2 * g.sb2;
   f32x16 acc = zero16();
-  for (int k0 = 0; k0 < g.K; k0 += KS) {
-    sgemm_stage<AK>(A, g.am, g.ak, g.M, g.K, m0, k0, As, LK);
-    sgemm_stage<BK>(B, g.bn, g.bk, g.N, g.K, n0, k0, Bs, LK);
+  for (int k0 = kbeg; k0 < kend; k0 += KS) {
+    sgemm_stage<AK>(A, g.am, g.ak, g.M, kend, m0, k0, As, LK);
+    sgemm_stage<BK>(B, g.bn, g.bk, g.N, kend, n0, k0, Bs, LK);
     __syncthreads();
 #pragma unroll
     for (int kc = 0; kc < KS; kc += 8) {
@@ -105,6 +113,16 @@ __global__ __launch_bounds__(256) void sgemm_kernel(SgemmArgs g) {
       Mma<float>::mma(acc, af, bf);
     }
     __syncthreads();
+  }
+  if (g.ksplit) {
+    float* P = (float*)g.part + (long)kz * g.M * g.N;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int m = m0 + wm * 32 + 8 * (j >> 2) + 4 * lg + (j & 3);
+      const int n = n0 + wn * 32 + l32;
+      if (m < g.M && n < g.N) P[(long)m * g.N + n] = acc[j];
+    }
+    return;
   }
   float* C = g.C + b1 * g.sc1 + b2 * g.sc2;
 #pragma unroll
@@ -137,7 +155,9 @@ __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __res
   __shared__ double Bs[KS][T + 1];
   const int tid = threadIdx.x;
   const int m0 = blockIdx.y * T, n0 = blockIdx.x * T;
-  const int b = blockIdx.z, b1 = b / g.nb2, b2 = b - b1 * g.nb2;
+  const int kz = g.ksplit ? (int)blockIdx.z : 0;
+  const int b = g.ksplit ? 0 : (int)blockIdx.z, b1 = b / g.nb2, b2 = b - b1 * g.nb2;
+  const int kbeg = kz * g.ksplit, kend = g.ksplit ? min(g.K, kbeg + g.ksplit) : g.K;
   const TA* A = A0 + b1 * g.sa1 + b2 * g.sa2;
   const TB* B = B0 + b1 * g.sb1 + b2 * g.sb2;
   const int lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
@@ -149,34 +169,36 @@ __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __res
     for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
   // the next k chunk's operands are loaded into registers while the current
   // chunk's MFMAs run (consecutive threads walk each operand's contiguous
-  // dimension)
-  double ra[PER], rb[PER];
+  // dimension); they stay in their own type until the LDS store, so that a
+  // conversion does not wait for the loads in front of the MFMAs
+  TA ra[PER];
+  TB rb[PER];
   auto load = [&](int k0) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = tid + 256 * u;
       const int r = AK ? e / KS : e % T, k = AK ? e % KS : e / T;
       const int gr = m0 + r, gk = k0 + k;
-      ra[u] = (gr < g.M && gk < g.K) ? (double)A[gr * g.am + gk * g.ak] : 0.0;
+      ra[u] = (gr < g.M && gk < kend) ? A[gr * g.am + gk * g.ak] : (TA)0;
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = tid + 256 * u;
       const int r = BK ? e / KS : e % T, k = BK ? e % KS : e / T;
       const int gr = n0 + r, gk = k0 + k;
-      rb[u] = (gr < g.N && gk < g.K) ? (double)B[gr * g.bn + gk * g.bk] : 0.0;
+      rb[u] = (gr < g.N && gk < kend) ? B[gr * g.bn + gk * g.bk] : (TB)0;
     }
   };
-  load(0);
-  for (int k0 = 0; k0 < g.K; k0 += KS) {
+  load(kbeg);
+  for (int k0 = kbeg; k0 < kend; k0 += KS) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int e = tid + 256 * u;
-      As[AK ? e % KS : e / T][AK ? e / KS : e % T] = ra[u];
-      Bs[BK ? e % KS : e / T][BK ? e / KS : e % T] = rb[u];
+      As[AK ? e % KS : e / T][AK ? e / KS : e % T] = (double)ra[u];
+      Bs[BK ? e % KS : e / T][BK ? e / KS : e % T] = (double)rb[u];
     }
     __syncthreads();
-    if (k0 + KS < g.K) load(k0 + KS);
+    if (k0 + KS < kend) load(k0 + KS);
 #pragma unroll
     for (int k = 0; k < KS; k += 4) {
       double av[2], bv[2];
@@ -191,6 +213,19 @@ __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __res
     }
     __syncthreads();
   }
+  if (g.ksplit) {
+    double* P = (double*)g.part + (long)kz * g.M * g.N;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int m = m0 + 32 * wm + 16 * i + lk + 4 * v, n = n0 + 32 * wn + 16 * j + li;
+          if (m < g.M && n < g.N) P[(long)m * g.N + n] = acc[i][j][v];
+        }
+    return;
+  }
   TC* C = C0 + b1 * g.sc1 + b2 * g.sc2;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -204,6 +239,23 @@ __global__ __launch_bounds__(256) void dgemm_kernel(SgemmArgs g, const TA* __res
         const double val = (double)g.alpha * acc[i][j][v] + (g.bias ? (double)g.bias[n] : 0.0);
         *c = (TC)(g.accumulate ? (double)*c + val : val);
       }
+}
+
+// Split-K epilogue: C(m, n) = alpha * sum_z part[z][m][n] (+ bias[n])
+// (+ C(m, n) if accumulate), the splits summed in order (deterministic).
+template <class TP, class TC>
+__global__ void ksplit_reduce_kernel(const TP* __restrict__ part, int splits, int M, int N, TC* __restrict__ C,
+                                     long ldc, double alpha, const float* __restrict__ bias, int accumulate) {
+  const long total = (long)M * N;
+  for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    double s = 0.0;
+    for (int z = 0; z < splits; ++z) s += (double)part[z * total + i];
+    const long m = i / N, n = i - m * N;
+    double v = alpha * s + (bias ? (double)bias[n] : 0.0);
+    TC* c = C + m * ldc + n;
+    if (accumulate) v += (double)*c;
+    *c = (TC)v;
+  }
 }
 
 // ---------------------------------------------------------------------------
