@@ -177,7 +177,7 @@ hipError_t sgemm(hipStream_t st, int M, int N, int K, Op A, Op B, float* C, long
   SgemmArgs g = gemm_args(M, N, K, A, B, C, ldc, acc, bias, bt, alpha);
   const int splits = ksplit_count(M, N, K, (long)bt.nb1 * bt.nb2);
   if (splits > 1) {
-    g.ksplit = (int)((((long)K + splits - 1) / splits + 15) / 16 * 16);
+    g.ksplit = (int)((((long)K + splits - 1) / splits + 31) / 32 * 32);
     g.part = t_kpart;
   }
   const int nz = splits > 1 ? (int)(((long)K + g.ksplit - 1) / g.ksplit) : bt.nb1 * bt.nb2;

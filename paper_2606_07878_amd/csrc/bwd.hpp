@@ -16,7 +16,8 @@ namespace still {
 //   C[b](m, n) = alpha * sum_k A[b](m, k) B[b](n, k)   (+ C[b](m, n) if accumulate)
 // with A[b](m, k) = A[b1 * sa1 + b2 * sa2 + m * am + k * ak], one of am, ak
 // equal to 1 (likewise B), b = b1 * nb2 + b2 the batch index, C row-major
-// with leading dimension ldc.  64 x 64 tiles, k stages of 16, four waves
+// with leading dimension ldc.  64 x 64 tiles, k stages of 32 (the next
+// stage loaded into registers during the current one's MFMAs), four waves
 // each owning one 32 x 32 MFMA tile; operands staged in LDS as [row][k].
 // ---------------------------------------------------------------------------
 struct SgemmArgs {
@@ -38,17 +39,19 @@ struct SgemmArgs {
   void* part;
 };
 
-// Stage a 64 x 16 tile (rows r0.., k k0..) of a strided operand into LDS
-// [64][LK].  K-contiguous sources load 4 consecutive k per thread, row-
-// contiguous sources 4 consecutive rows; edges fall back to scalar loads.
+// Load this thread's part of a 64 x 16 tile (rows r0.., k k0..) of a
+// strided operand (k < K, rows < R; zeros outside) into registers, and store
+// it into LDS [64][LK].  K-contiguous sources: 4 consecutive k per thread;
+// row-contiguous sources: 4 consecutive rows; edges fall back to scalar loads.
 template <bool KCONT>
-__device__ __forceinline__ void sgemm_stage(const float* __restrict__ X, long xr, long xk, int R, int K, int r0,
-                                            int k0, float* __restrict__ S, int LK) {
+__device__ __forceinline__ void sgemm_load(const float* __restrict__ X, long xr, long xk, int R, int K, int r0,
+                                           int k0, float (&v)[4]) {
   const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = 0.f;
   if (KCONT) {
     const int r = tid >> 2, k = (tid & 3) * 4;
     const int gr = r0 + r, gk = k0 + k;
-    float v[4] = {0.f, 0.f, 0.f, 0.f};
     if (gr < R) {
       const float* p = X + gr * xr + gk;
       if (gk + 3 < K && ((uintptr_t)p & 15u) == 0) {
@@ -63,12 +66,9 @@ __device__ __forceinline__ void sgemm_stage(const float* __restrict__ X, long xr
           if (gk + i < K) v[i] = p[i];
       }
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) S[r * LK + k + i] = v[i];
   } else {
     const int k = tid >> 4, r = (tid & 15) * 4;
     const int gr = r0 + r, gk = k0 + k;
-    float v[4] = {0.f, 0.f, 0.f, 0.f};
     if (gk < K) {
       const float* p = X + gk * xk + gr;
       if (gr + 3 < R && ((uintptr_t)p & 15u) == 0) {
@@ -83,6 +83,17 @@ __device__ __forceinline__ void sgemm_stage(const float* __restrict__ X, long xr
           if (gr + i < R) v[i] = p[i];
       }
     }
+  }
+}
+template <bool KCONT>
+__device__ __forceinline__ void sgemm_store(const float (&v)[4], float* __restrict__ S, int LK) {
+  const int tid = threadIdx.x;
+  if (KCONT) {
+    const int r = tid >> 2, k = (tid & 3) * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) S[r * LK + k + i] = v[i];
+  } else {
+    const int k = tid >> 4, r = (tid & 15) * 4;
 #pragma unroll
     for (int i = 0; i < 4; ++i) S[(r + i) * LK + k] = v[i];
   }
@@ -90,7 +101,7 @@ __device__ __forceinline__ void sgemm_stage(const float* __restrict__ X, long xr
 
 template <bool AK, bool BK>
 __global__ __launch_bounds__(256) void sgemm_kernel(SgemmArgs g) {
-  constexpr int T = 64, KS = 16, LK = KS + 4;
+  constexpr int T = 64, KS = 32, LK = KS + 4;   // k stage = two 16-wide halves
   __shared__ __attribute__((aligned(16))) float As[T * LK];
   __shared__ __attribute__((aligned(16))) float Bs[T * LK];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -102,10 +113,24 @@ __global__ __launch_bounds__(256) void sgemm_kernel(SgemmArgs g) {
   const float* A = g.A + b1 * g.sa1 + b2 * g.sa2;
   const float* B = g.B + b1 * g.sb1 + b2 * g.sb2;
   f32x16 acc = zero16();
+  // the next k stage is loaded into registers while the current one's MFMAs run
+  float ra[2][4], rb[2][4];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      sgemm_load<AK>(A, g.am, g.ak, g.M, kend, m0, k0 + 16 * h, ra[h]);
+      sgemm_load<BK>(B, g.bn, g.bk, g.N, kend, n0, k0 + 16 * h, rb[h]);
+    }
+  };
+  load(kbeg);
   for (int k0 = kbeg; k0 < kend; k0 += KS) {
-    sgemm_stage<AK>(A, g.am, g.ak, g.M, kend, m0, k0, As, LK);
-    sgemm_stage<BK>(B, g.bn, g.bk, g.N, kend, n0, k0, Bs, LK);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      sgemm_store<AK>(ra[h], As + 16 * h, LK);
+      sgemm_store<BK>(rb[h], Bs + 16 * h, LK);
+    }
     __syncthreads();
+    if (k0 + KS < kend) load(k0 + KS);
 #pragma unroll
     for (int kc = 0; kc < KS; kc += 8) {
       const f32x4 af = *(const f32x4*)&As[(wm * 32 + l32) * LK + kc + 4 * lg];
