@@ -480,6 +480,8 @@ def main():
                     help="skip the decode-attention measurement (shorter profiler runs)")
     ap.add_argument("--summarize-counters", metavar="CSV",
                     help="print per-kernel means of a rocprofv3 counter-collection CSV and exit (no GPU use)")
+    ap.add_argument("--backward-only", action="store_true",
+                    help="time only the backward pass of one layer (the 'backward' object) and print that object")
     ap.add_argument("--library-gemm-reference", action="store_true",
                     help="time the vendor library's fp16 product (torch.bmm) on the latent-side product shapes "
                          "of --workload and print that object (reference for the MFMA rate, no compaction)")
@@ -502,6 +504,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.copy_probe_mib:
         copy_probe(args.copy_probe_mib, dev)
+    if args.backward_only:
+        print(json.dumps({"backward": backward_measure(args.workload, dev, binding)}), flush=True)
+        return
     if args.library_gemm_reference:
         w = configs.get_workload(args.workload)
         print(json.dumps({"library_gemm_reference": library_gemm_reference(args.workload, dev),
