@@ -76,6 +76,14 @@ def test_self_attention_head_widths(ds, t):
     _case(configs.shrink(W1, self_head_dim=ds), N=1000, t=t, name=f"cfg1 d_s={ds} t={t}")
 
 
+@pytest.mark.parametrize("dc,t", [(384, 300), (640, 129), (256, 1)])
+def test_cross_head_widths(dc, t):
+    """Cross heads dc wide on the cfg-1 cache: 6 and 10 query chunks of 64 per
+    head, so the query-stage ring wraps inside a key block (4 stages), and 4
+    chunks (one ring turn per block); ragged t."""
+    _case(configs.shrink(W1, cross_head_dim=dc), N=1000, t=t, name=f"cfg1 d_c={dc} t={t}")
+
+
 @pytest.mark.parametrize("mode", [pytest.param(configs.MODE_BF16, marks=MULTI_BLOCK_XFAIL), configs.MODE_FP32])
 def test_config1_two_blocks_gelu_final_norm(mode):
     _case(configs.shrink(W1, n_blocks=2, ffn_kind=configs.FFN_GELU, final_norm=1), mode=mode,
