@@ -9,9 +9,11 @@
 * the identity-style initialisation of Appendix C at t = T (the paper's only
   end-to-end closed form: compact cache == original cache);
 * an independent pure-Python loop evaluation of a whole layer on tiny inputs;
-* Appendix D's parameter count and Appendix B's KV-size figures as printed.
+* Appendix D's parameter count and Appendix B's KV-size figures as printed
+  (fixtures under tests/golden, each citing where the paper gives it).
 """
 import math
+import os
 
 import numpy as np
 import pytest
@@ -362,28 +364,63 @@ def _count(cfg, t):
     return n + cfg.latent_dim      # + the optional beta head w_beta in R^{d_l}
 
 
-@pytest.mark.parametrize("B,Bc,nc,ns,r,t,printed", [
-    (2, 2, 1, 1, 0, 128, 50e6),     # canonical Qwen3-4B compactor
-    (4, 1, 8, 8, 4, 140, 466e6),    # first-block-only cross-attention
-    (4, 4, 8, 8, 4, 140, 692e6),    # cross-attention every block
-])
-def test_parameter_count_appendix_d(B, Bc, nc, ns, r, t, printed):
-    L, H, d, dl = 36, 8, 128, 256
-    cfg = configs.CompactorConfig(n_kv_heads=H, head_dim=d, latent_dim=dl, n_blocks=B,
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden_rows(name):
+    """Whitespace-separated rows of a fixture under tests/golden (comments dropped)."""
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.split("#", 1)[0].split()
+            if line:
+                rows.append(line)
+    return rows
+
+
+_PARAM_ROWS = [r for r in _golden_rows("appendix_d_parameter_counts.txt") if r[0] != "bf16_canonical"]
+_L, _H, _D, _DL = 36, 8, 128, 256   # Qwen3-4B-shaped base model and d_l of the printed configurations
+
+
+def _formula(row):
+    t, B, Bc, nc, ns, r = (int(v) for v in row[:6])
+    return sizing.compactor_params_per_layer(_H, t, _D, _DL, B, Bc, nc, ns, r, ffn=bool(r))
+
+
+@pytest.mark.parametrize("row", _PARAM_ROWS, ids=[r[6] for r in _PARAM_ROWS])
+def test_parameter_count_appendix_d(row):
+    """App. D totals: the formula, the oracle's own tensor shapes and the printed figure agree."""
+    t, B, Bc, nc, ns, r = (int(v) for v in row[:6])
+    printed, tol = float(row[6]), float(row[7])
+    cfg = configs.CompactorConfig(n_kv_heads=_H, head_dim=_D, latent_dim=_DL, n_blocks=B,
                                   cross_every_block=int(Bc == B), n_cross_heads=nc, n_self_heads=ns,
                                   ffn_kind=configs.FFN_GELU if r else configs.FFN_NONE,
-                                  ffn_hidden=r * dl)
-    formula = sizing.compactor_params_per_layer(H, t, d, dl, B, Bc, nc, ns, r, ffn=bool(r))
+                                  ffn_hidden=r * _DL)
+    formula = _formula(row)
     assert _count(cfg, t) == formula
-    assert abs(L * formula - printed) / printed < 0.01
+    assert abs(_L * formula - printed) / printed < tol
+
+
+def test_canonical_bf16_bytes_appendix_b():
+    """App. B: the canonical compactor's bf16 storage, from its App. D count."""
+    (mib_row,) = [r for r in _golden_rows("appendix_d_parameter_counts.txt") if r[0] == "bf16_canonical"]
+    printed, tol = float(mib_row[1]), float(mib_row[2])
+    canonical = _PARAM_ROWS[0]
+    assert abs(_L * _formula(canonical) * 2 / 2 ** 20 - printed) / printed < tol
 
 
 def test_kv_bytes_appendix_b():
-    per_tok = sizing.kv_bytes(36, 8, 128, 2, 1)
-    assert per_tok == 144 * 1024
-    for S, gib in [(8192, 1.125), (32768, 4.5), (65536, 9.0), (131072, 18.0)]:
-        assert sizing.kv_bytes(36, 8, 128, 2, S) == gib * 2 ** 30
-    assert abs(sizing.kv_bytes(36, 8, 128, 2, 328) / 2 ** 20 - 46) < 0.5
+    """App. B: M_KV(S) = 2 L H_kv d b S for the Qwen3-4B-shaped cache, against the printed sizes."""
+    unit = {"KiB": 2 ** 10, "MiB": 2 ** 20, "GiB": 2 ** 30}
+    rows = _golden_rows("appendix_b_kv_footprint.txt")
+    assert len(rows) == 6
+    for _, S, printed, u, tol in rows:
+        got = sizing.kv_bytes(36, 8, 128, 2, int(S)) / unit[u]
+        want = float(printed)
+        if float(tol) == 0:
+            assert got == want
+        else:
+            assert abs(got - want) / want < float(tol)
 
 
 # --------------------------------------------------------------------------- Appendix B compositions
