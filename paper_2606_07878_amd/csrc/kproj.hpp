@@ -19,7 +19,9 @@
 // Workgroup = KPW key positions x all H KV heads (128 rows, KPW = 128 / H),
 // 4 waves.  The X rows stay in LDS for the whole workgroup; the rotation
 // table rows of the KPW positions are staged in LDS per tile of 32 pairs and
-// shared by all cross heads and KV heads.  Wave w takes the cross heads
+// shared by all cross heads and KV heads, and so are the tile's b_K values
+// (the epilogue then has no global loads to wait for: on gfx9 such a wait
+// also waits for the wave's earlier key stores).  Wave w takes the cross heads
 // c = w, w + 4, ...; W_K comes from a fragment-tiled fp16 copy (wtile_off).
 #pragma once
 #include "common.hpp"
@@ -75,6 +77,9 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
   // different LDS banks (a 256-byte stride maps every row to one bank group)
   constexpr int TS = 34;
   __shared__ __attribute__((aligned(16))) float2 Ts[2 * TPW * TS];
+  // bias stage: per buffer, the 8 cross heads 4 cb .. 4 cb + 7 of the current
+  // pair round, widths 32 p .. 32 p + 31 of each RoPE half (4 values per uint2)
+  __shared__ uint2 Bs[2][8][16];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -95,7 +100,15 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
   }
   // rotation tile: (cos, sin) of key positions n0 .. n0 + kpw - 1 for pairs
   // 32p .. 32p + 31, computed from the fp64 positions and frequencies
-  auto load_tab = [&](int p, int buf) {
+  const TBias* bias = (const TBias*)a.bias;
+  auto load_tab = [&](int p, int buf, int cbv) {
+    if (tid < 128) {
+      const int lc = tid >> 4, u = tid & 15, c = 4 * cbv + lc;
+      uint2 val = make_uint2(0, 0);
+      if (bias && c < a.nc)
+        val = *(const uint2*)(bias + (long)c * a.dc + (u < 8 ? 32 * p + 4 * u : hh + 32 * p + 4 * (u - 8)));
+      Bs[buf][lc][u] = val;
+    }
     for (int v = tid; v < kpw * 16; v += 256) {
       const int pos = v >> 4, j2 = (v & 15) * 2;
       const int n = n0 + pos;
@@ -108,7 +121,7 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
       *(f32x4*)&Ts[(buf * kpw + pos) * TS + j2] = cs;
     }
   };
-  load_tab(0, 0);
+  load_tab(0, 0, 0);
 
   // this lane's key in each key tile: row, KV head, key index
   int kh[4], kn[4];
@@ -134,7 +147,6 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
       ss[kt] = 0.f;
     }
   };
-  const TBias* bias = (const TBias*)a.bias;
 
   int tb = 0;   // table buffer of the current tile
   for (int cb = 0; cb < rounds; cb += 2) {   // pairs of this wave's cross heads
@@ -142,8 +154,8 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
     for (int kt = 0; kt < 4; ++kt) ss0[kt] = ss1[kt] = 0.f;
     for (int p = 0; p < NPT; ++p) {
       __syncthreads();                       // X rows / table tile p visible; the other buffer free
-      if (p + 1 < NPT) load_tab(p + 1, tb ^ 1);
-      else if (cb + 2 < rounds) load_tab(0, tb ^ 1);   // the next pair of cross heads restarts at tile 0
+      if (p + 1 < NPT) load_tab(p + 1, tb ^ 1, cb);
+      else if (cb + 2 < rounds) load_tab(0, tb ^ 1, cb + 2);   // the next pair of cross heads restarts at tile 0
       const float2* T = Ts + (size_t)tb * kpw * TS;
 #pragma unroll 1
       for (int i = 0; i < 2; ++i) {
@@ -183,16 +195,13 @@ __global__ __launch_bounds__(256, 2) void kproj_kernel(KprojArgs a) {
         // biases of this lane's widths: 4 consecutive values per group q (8-byte loads)
         static_assert(sizeof(TBias) == 2, "2-byte bias type");
         uint2 bl[4], bu[4];
-        if (bias) {
-          const TBias* bc = bias + (long)c * a.dc + 32 * p + 4 * g;
+        {
+          const uint2* bsrc = &Bs[tb][c - 4 * cb][0];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            bl[q] = *(const uint2*)(bc + 8 * q);
-            bu[q] = *(const uint2*)(bc + hh + 8 * q);
+            bl[q] = bsrc[2 * q + g];
+            bu[q] = bsrc[8 + 2 * q + g];
           }
-        } else {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) bl[q] = bu[q] = make_uint2(0, 0);
         }
         auto bias_at = [&](const uint2& v, int u) -> float {
           const uint32_t wd = u < 2 ? v.x : v.y;
