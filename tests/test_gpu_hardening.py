@@ -16,8 +16,8 @@
 * The App. C identity-style initialisation at t = N on the GPU: the compact
   cache reproduces the input cache.
 * A workspace filled with NaN bit patterns before the call, at ragged N and t
-  (key tiles past N and past t are padding): nothing stale may reach the
-  outputs.
+  (key tiles past N and past t are padding), for the cfg-1 compactor and the
+  Qwen-8B-shaped one: nothing stale may reach the outputs.
 """
 import math
 
@@ -281,25 +281,44 @@ def test_large_cache_magnitudes(wid, outlier, vscale, N, t):
                       what=f"large magnitudes cfg{wid} K x{outlier:g} V x{vscale:g} mode{mode}")
 
 
+def _poisoned_case(w, N, t, mode, tol, heads=None):
+    """One layer with the workspace filled with all-ones bytes (NaN in fp16
+    and fp32) before the call, against the oracle."""
+    import torch
+    from paper_2606_07878_amd import binding
+    cache = synth.make_cache(w, 0, n_tokens=N)
+    wts = synth.make_weights(w, 0, t=t)
+    log(f"case poisoned workspace: {w.name} N={N} t={t} mode {mode}")
+    need = binding.still_workspace_size(binding.make_config(w.cfg, mode), N, t, 1)
+    ws = torch.full((need,), 255, dtype=torch.uint8, device="cuda")
+    K = dev_tensor(cache["K"], mode)
+    V = dev_tensor(cache["V"], mode)
+    pos = torch.from_numpy(cache["positions"]).cuda()
+    W = {k: dev_tensor(v, mode) for k, v in wts.items()}
+    Ck, Cv, p = binding.compact_layer(w.cfg, W, K, V, pos, w.rope_theta, t, mode=mode, workspace=ws)
+    torch.cuda.synchronize()
+    got = (Ck.double().cpu().numpy(), Cv.double().cpu().numpy(), p.cpu().numpy())
+    if heads is not None:
+        got = (got[0][heads], got[1][heads], got[2])
+    ref = run_oracle(w.cfg, cache, wts, w.rope_theta, t, heads=heads)
+    assert_parity(got, ref, tol, what=f"N={N} t={t} poisoned workspace mode{mode}")
+
+
 @pytest.mark.parametrize("mode,tol", MODES)
 def test_poisoned_workspace_ragged_shapes(mode, tol):
     """cfg-1 compactor (flash self-attention, d_s = 128) at N = 1000, t = 300:
     the cross-attention's last key tile and the self-attention's last latent
     tile are partly padding; the workspace starts as all-ones bytes (NaN in
     fp16 and fp32)."""
-    import torch
-    from paper_2606_07878_amd import binding
-    N, t = 1000, 300
-    cache = synth.make_cache(W1, 0, n_tokens=N)
-    wts = synth.make_weights(W1, 0, t=t)
-    need = binding.still_workspace_size(binding.make_config(W1.cfg, mode), N, t, 1)
-    ws = torch.full((need,), 255, dtype=torch.uint8, device="cuda")
-    K = dev_tensor(cache["K"], mode)
-    V = dev_tensor(cache["V"], mode)
-    pos = torch.from_numpy(cache["positions"]).cuda()
-    W = {k: dev_tensor(v, mode) for k, v in wts.items()}
-    Ck, Cv, p = binding.compact_layer(W1.cfg, W, K, V, pos, W1.rope_theta, t, mode=mode, workspace=ws)
-    torch.cuda.synchronize()
-    got = (Ck.double().cpu().numpy(), Cv.double().cpu().numpy(), p.cpu().numpy())
-    ref = run_oracle(W1.cfg, cache, wts, W1.rope_theta, t)
-    assert_parity(got, ref, tol, what=f"cfg1 N={N} t={t} poisoned workspace mode{mode}")
+    _poisoned_case(W1, 1000, 300, mode, tol)
+
+
+@pytest.mark.parametrize("N,t", [(1000, 300), (4097, 129)])
+@pytest.mark.parametrize("mode,tol", MODES)
+def test_poisoned_workspace_ragged_qwen_shape(N, t, mode, tol):
+    """The Qwen-8B-shaped compactor (8 KV heads of width 128, D = 1024, 8 + 8
+    heads of width 1024) at ragged N and t: the key projection's workgroups of
+    16 keys x 8 KV heads end inside the cache, the 256-key blocks of the
+    cross-attention (2d = 256) end in padding, the wide self-attention's
+    score rows end in padding; the workspace starts as NaN bit patterns."""
+    _poisoned_case(W2, N, t, mode, tol, heads=[0, 7])
