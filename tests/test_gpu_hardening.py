@@ -322,3 +322,11 @@ def test_poisoned_workspace_ragged_qwen_shape(N, t, mode, tol):
     cross-attention (2d = 256) end in padding, the wide self-attention's
     score rows end in padding; the workspace starts as NaN bit patterns."""
     _poisoned_case(W2, N, t, mode, tol, heads=[0, 7])
+
+
+@pytest.mark.parametrize("mode,tol", MODES)
+def test_poisoned_workspace_ragged_wide_heads(mode, tol):
+    """The 64k-cache stack's compactor (8 KV heads of width 256, so 2d = 512:
+    64-latent cross-attention tiles, the d = 256 refinement and key
+    projection; D = 2048) at N = 1000, t = 300, NaN-poisoned workspace."""
+    _poisoned_case(configs.get_workload(5), 1000, 300, mode, tol, heads=[0, 7])
