@@ -493,8 +493,9 @@ def main():
         summarize_counters(args.summarize_counters)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the compactor forward runs on a "
-              "single MI355X in this build.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the library runs a layer on one "
+              "MI355X and has no multi-GPU path; a layer's KV heads or the layers of a stack would be "
+              "spread over GPUs by the caller.", file=sys.stderr)
         sys.exit(2)
 
     import torch
