@@ -48,7 +48,7 @@ struct AttnArgs {
 // Overflow capacity per (split, latent row) of the fp16 kernel: in-margin keys
 // that a full register list rejects or evicts (exact ties of duplicated cache
 // rows, or more near-maximal keys per lane than the list holds).
-constexpr int XATT_OVF = 128;
+constexpr int XATT_OVF = 384;
 
 template <class CT, int TT, int NB, int DK, int D2, int TOPK>
 __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {

@@ -114,7 +114,7 @@ constexpr int XATT_KB = 256;   // keys per block of the fp16 cross-attention ker
 constexpr int XATT_TOPK = 4;   // keys tracked per (latent, wave, lane half) by the fp16 kernel
 // keys per latent whose logits are recomputed accurately: every candidate
 // within the refinement margin, up to this many
-constexpr int REFINE_R = 64;
+constexpr int REFINE_R = 256;
 static_assert(REFINE_R <= REFINE_RMAX, "merge_kernel handles up to REFINE_RMAX refined keys per latent");
 // refinement rows per list the fp16 refinement grid covers at once (its
 // workgroups loop over further tiles): about 4 per latent

@@ -443,7 +443,9 @@ __global__ __launch_bounds__(256) void softmax_rows_kernel(const float* __restri
 // Pick, per latent row, every candidate of the flash pass's per-split lists
 // whose logit lies within REFINE_MARGIN of the row maximum, largest first, up
 // to R of them: slots [0, rcnt[row]) of the row hold them.  Exact ties (duplicated
-// cache rows) are all taken, so their weights stay consistent.  A split's
+// cache rows) are taken together up to that cap, so their weights stay
+// consistent.  More than CAP in-margin entries in a row: the first CAP read
+// are ranked.  A split's
 // list of C entries holds CB fixed entries, then (with ocnt) ocnt[split][row]
 // overflow entries.
 //
@@ -459,7 +461,7 @@ __global__ __launch_bounds__(256) void refine_select_kernel(const float* __restr
                                                             const float* __restrict__ mpart, int S, long HCT, int C,
                                                             int CB, int* __restrict__ ridx, float* __restrict__ rval,
                                                             int* __restrict__ rcnt) {
-  constexpr int CAP = 256;   // in-margin candidates kept per row
+  constexpr int CAP = 512;   // in-margin candidates kept per row
   __shared__ float sv[4][CAP];
   __shared__ int si[4][CAP];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -549,7 +551,7 @@ static __global__ __launch_bounds__(256) void refine_compact_kernel(const int* _
 // where, for each refined key r, D_r = 2^(S_exact - M) - 2^(S_flash - M) swaps
 // the weight the flash pass gave it for the accurate one (R = 0: plain merge).
 // Slots [0, rcnt[row]) of a row hold its refined keys.
-constexpr int REFINE_RMAX = 64;   // refined keys per latent the merge handles (one per lane)
+constexpr int REFINE_RMAX = 256;  // refined keys per latent the merge handles (64 per pass of a wave)
 struct RefineArgs {
   int R, NP;
   const int* ridx;          // [H*nc*t][R]
@@ -568,8 +570,10 @@ struct RefineArgs {
 // One wave per output row (h, c, i); lane l owns features [l*VPL, (l+1)*VPL).
 // All loads that do not depend on one another are issued before any result
 // is used: the first split's partial row, every split's (m, l), and the
-// refined keys' indices, flash logits and exact-logit data; the rows of X of
-// the refined keys follow, four at a time, once their indices are known.
+// first 64 refined keys' indices, flash logits and exact-logit data (one key
+// per lane); the rows of X of the refined keys follow, four at a time, once
+// their indices are known.  Rows with more refined keys take them 64 at a
+// time afterwards.
 template <class CT, int VPL>
 __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ opart, const float* __restrict__ mpart,
                                                     const float* __restrict__ lpart, int S, int H, int nc, int t,
@@ -601,13 +605,16 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
   int key = -1;
   float rv = 0.f, dot = 0.f, ss = 0.f;
   const int nref = ra.R > 0 ? ra.rcnt[row] : 0;
-  if (lane < nref) {
-    key = ra.ridx[row * ra.R + lane];
-    rv = ra.rval[row * ra.R + lane];
+  const int n0 = min(nref, 64);
+  auto ref_load = [&](int r, int& key, float& rv, float& dot, float& ss) {
+    dot = 0.f;
+    ss = 0.f;
+    key = ra.ridx[row * ra.R + r];
+    rv = ra.rval[row * ra.R + r];
     if (ra.NP == 0) {
-      dot = ra.rpart[row * ra.R + lane].x;
+      dot = ra.rpart[row * ra.R + r].x;
     } else {
-      const float2* p = ra.rpart + (row * ra.R + lane) * ra.NP;
+      const float2* p = ra.rpart + (row * ra.R + r) * ra.NP;
       float d1 = 0.f, s1 = 0.f;
       int k = 0;
       for (; k + 1 < ra.NP; k += 2) {
@@ -624,7 +631,8 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
       dot += d1;
       ss += s1;
     }
-  }
+  };
+  if (lane < n0) ref_load(lane, key, rv, dot, ss);
   const float rqv = ra.R > 0 && ra.NP > 0 ? ra.rq[((long)h * t + i) * nc + c] : 0.f;
   // maximum and normaliser over the splits
   float M = ms_l;
@@ -637,42 +645,54 @@ __global__ __launch_bounds__(256) void merge_kernel(const float* __restrict__ op
     if (ms != -INFINITY) L += exp2f(ms - M) * lpart[s * HCT + row];
   }
   // weight change of each refined key: 2^(exact - M) - 2^(flash - M)
-  float dl = 0.f;
-  if (lane < nref) {
-    if (ra.NP == 0) {
-      dl = exp2f(rv - M) * expm1f(dot * 0.69314718055994531f);
-    } else {
-      const float sx = ra.scale_log2 * rqv * dot / fmaxf(sqrtf(ss), ra.l2_eps);
-      dl = exp2f(sx - M) - exp2f(rv - M);
-    }
-  }
+  auto delta = [&](float rv, float dot, float ss) -> float {
+    if (ra.NP == 0) return exp2f(rv - M) * expm1f(dot * 0.69314718055994531f);
+    const float sx = ra.scale_log2 * rqv * dot / fmaxf(sqrtf(ss), ra.l2_eps);
+    return exp2f(sx - M) - exp2f(rv - M);
+  };
+  float dl = lane < n0 ? delta(rv, dot, ss) : 0.f;
   L += dl;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
   const float w0 = __shfl(ms_l, 0);
   float acc[VPL];
   const float ws0 = w0 != -INFINITY ? exp2f(w0 - M) : 0.f;
 #pragma unroll
   for (int u = 0; u < VPL; ++u) acc[u] = ws0 * v0[u];
-  // refined keys' rows of X, four at a time
-  for (int r0 = 0; r0 < nref; r0 += 4) {
-    float xr[4][VPL];
-    float dr[4];
+  // refined keys' rows of X, four at a time; keys cb .. cb + nk - 1 held by
+  // lanes 0 .. nk - 1 (key index, weight change)
+  auto add_rows = [&](int nk) {
+    for (int r0 = 0; r0 < nk; r0 += 4) {
+      float xr[4][VPL];
+      float dr[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int n = __shfl(key, r0 + q);
-      dr[q] = __shfl(dl, r0 + q);
-      const bool use = r0 + q < nref;
-      const CT* x = (const CT*)ra.X + ((long)h * ra.N + (use ? n : 0)) * d2 + f0;
+      for (int q = 0; q < 4; ++q) {
+        const int n = __shfl(key, r0 + q);
+        dr[q] = __shfl(dl, r0 + q);
+        const bool use = r0 + q < nk;
+        const CT* x = (const CT*)ra.X + ((long)h * ra.N + (use ? n : 0)) * d2 + f0;
 #pragma unroll
-      for (int u = 0; u < VPL; ++u) xr[q][u] = to_f32(x[u]);
-      if (!use) dr[q] = 0.f;
+        for (int u = 0; u < VPL; ++u) xr[q][u] = to_f32(x[u]);
+        if (!use) dr[q] = 0.f;
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int u = 0; u < VPL; ++u) acc[u] += dr[q] * xr[q][u];
     }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int u = 0; u < VPL; ++u) acc[u] += dr[q] * xr[q][u];
+  };
+  add_rows(n0);
+  for (int cb = 64; cb < nref; cb += 64) {   // rows with more than 64 refined keys
+    const int nk = min(nref - cb, 64);
+    key = -1;
+    dl = 0.f;
+    if (lane < nk) {
+      ref_load(cb + lane, key, rv, dot, ss);
+      dl = delta(rv, dot, ss);
+    }
+    L += dl;
+    add_rows(nk);
   }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
   for (int s = 1; s < S; ++s) {
     const float ms = mpart[s * HCT + row];
     if (ms == -INFINITY) continue;
