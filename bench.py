@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0
 # from rocprofv3 PMC FETCH_SIZE / WRITE_SIZE passes scaled by what the same
 # counters read for a 1 GiB device copy (factors 2.0 and 1.0).  Valid only for
 # the kernel sources with this digest; any later change reports null.
-MEASURED_TRAFFIC = {"workload": 2, "sources_sha256_16": "10e2cd9371651cb1", "bytes_per_launch": 5559172403}
+MEASURED_TRAFFIC = {"workload": 2, "sources_sha256_16": "2b19019e08584c64", "bytes_per_launch": 5556192768}
 KERNEL_SOURCES = ("paper_2606_07878_amd/csrc/attn.hpp", "paper_2606_07878_amd/csrc/common.hpp")
 
 

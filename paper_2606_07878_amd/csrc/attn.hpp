@@ -40,15 +40,21 @@ struct AttnArgs {
   float scale_log2;  // logit scale * log2(e)
   int keys_per_split;
   float* cval;       // TOPK > 0: [S][H*nc][t][ncand] largest logits seen (log2 units) ...
-  int* cidx;         // ... and their key indices (-1 = none), per half-lane; fp16 kernel:
-                     // [0, NBK*TOPK) the per-bucket lists, then up to XATT_OVF overflow entries
-  int* ocnt;         // fp16 kernel: [S][H*nc][t] overflow entries written per row
+  int* cidx;         // ... and their key indices (-1 = none): the per-list entries (fp32
+                     // kernel: 2 TOPK, one list per lane half; fp16 kernel: NBK*TOPK, one
+                     // per bucket), then up to ATT_OVF / XATT_OVF overflow entries
+  int* ocnt;         // [S][H*nc][t] overflow entries written per row
 };
 
-// Overflow capacity per (split, latent row) of the fp16 kernel: in-margin keys
-// that a full register list rejects or evicts (exact ties of duplicated cache
-// rows, or more near-maximal keys per lane than the list holds).
-constexpr int XATT_OVF = 384;
+// Overflow capacity per (split, latent row): in-margin keys that a full
+// register list rejects or evicts (exact ties of duplicated cache rows, or
+// more near-maximal keys per lane than the list holds).  Keys enter while
+// they are within the margin of the running maximum, so early blocks can
+// fill it with keys that a later, larger maximum leaves outside the margin;
+// the capacity is sized for that (a cache of 32-fold duplicated rows writes
+// several hundred entries to some rows).
+constexpr int XATT_OVF = 1536;   // fp16 kernel
+constexpr int ATT_OVF = 1536;    // fp32 kernel
 
 template <class CT, int TT, int NB, int DK, int D2, int TOPK>
 __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
@@ -70,6 +76,7 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) CT Ks[2][NB * LQ];
   __shared__ __attribute__((aligned(16))) CT Xs[D2 * LX];
   __shared__ float rks[NB];
+  __shared__ int ovn[TT];   // overflow entries of each latent row
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, lg = lane >> 5;
@@ -87,6 +94,9 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
   const int my_lat = t0 + wave * 32 + l32;
   const float rq = my_lat < a.t ? a.rq[((long)h * a.t + my_lat) * a.nc + c] : 0.f;
   const float qscale = rq * a.scale_log2;
+  if (tid < TT) ovn[tid] = 0;   // read after the first block's barriers
+  constexpr int NCAND = 2 * (TOPK > 0 ? TOPK : 1) + ATT_OVF;   // list entries per (split, row)
+  const long crow_ = ((long)split * a.H * a.nc + hc) * a.t + my_lat;
 
   f32x16 o[FT];
 #pragma unroll
@@ -185,20 +195,39 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
         s[kt][j] = x;
         mx = fmaxf(mx, x);
         if constexpr (TOPK > 0) {
-          if (x > tv[TOPK - 1]) {
-            float v = x;
-            int id = n0 + kl;
-            bool moved = false;   // entries after the insertion point shift (exact ties too)
+          // keys within REFINE_MARGIN of the running maximum enter the lane's
+          // sorted list; the entry a full list pushes out, or the key itself
+          // when it does not enter, goes to the row's overflow list if it is
+          // still in the margin (padding rows past t take none)
+          const float cut = fmaxf(m_run, mx) - REFINE_MARGIN;
+          if (x > cut && my_lat < a.t) {
+            auto overflow = [&](float ov, int ok) {
+              const int slot = atomicAdd(&ovn[wave * 32 + l32], 1);
+              if (slot < ATT_OVF) {
+                a.cval[crow_ * NCAND + 2 * TOPK + slot] = ov;
+                a.cidx[crow_ * NCAND + 2 * TOPK + slot] = ok;
+              }
+            };
+            if (x > tv[TOPK - 1]) {
+              const float ev = tv[TOPK - 1];
+              const int ek = ti[TOPK - 1];
+              float v = x;
+              int id = n0 + kl;
+              bool moved = false;   // entries after the insertion point shift (exact ties too)
 #pragma unroll
-            for (int q = 0; q < TOPK; ++q) {
-              const bool gt = moved || v > tv[q];
-              const float tvq = tv[q];
-              const int tiq = ti[q];
-              tv[q] = gt ? v : tvq;
-              ti[q] = gt ? id : tiq;
-              v = gt ? tvq : v;
-              id = gt ? tiq : id;
-              moved = gt;
+              for (int q = 0; q < TOPK; ++q) {
+                const bool gt = moved || v > tv[q];
+                const float tvq = tv[q];
+                const int tiq = ti[q];
+                tv[q] = gt ? v : tvq;
+                ti[q] = gt ? id : tiq;
+                v = gt ? tvq : v;
+                id = gt ? tiq : id;
+                moved = gt;
+              }
+              if (ek >= 0 && ev > cut) overflow(ev, ek);
+            } else {
+              overflow(x, n0 + kl);
             }
           }
         }
@@ -276,9 +305,10 @@ __global__ __launch_bounds__(256) void cross_attn_kernel(AttnArgs a) {
     if constexpr (TOPK > 0) {
 #pragma unroll
       for (int q = 0; q < TOPK; ++q) {
-        a.cval[row * (2 * TOPK) + lg * TOPK + q] = tv[q];
-        a.cidx[row * (2 * TOPK) + lg * TOPK + q] = ti[q];
+        a.cval[row * NCAND + lg * TOPK + q] = tv[q];
+        a.cidx[row * NCAND + lg * TOPK + q] = ti[q];
       }
+      if (lg == 0) a.ocnt[row] = min(ovn[wave * 32 + l32], ATT_OVF);
     }
   }
 }

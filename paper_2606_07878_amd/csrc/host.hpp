@@ -131,7 +131,7 @@ struct Dims {
   int np_c, np_s;       // sum-of-squares partials per (row, head)
   int topk, R;          // logit refinement
   int ncand;            // candidate slots per (split, latent row) written by the attention kernel
-  int ncand_fixed;      // ... of which the per-bucket lists (fp16 kernel: then up to XATT_OVF overflow entries)
+  int ncand_fixed;      // ... of which the fixed lists (then up to ATT_OVF / XATT_OVF overflow entries)
   int att_tt;           // latents per attention workgroup
   int splits;           // split-N factor of the cross-attention
   long keys_per_split;
@@ -223,7 +223,7 @@ inline still_status make_dims(const still_config* c, int64_t N, int32_t t, Dims*
   m->np_s = m->ns > 0 ? m->ds / GEMM_BN * 2 : 0;
   m->topk = m->fp32 ? ATT_TOPK : XATT_TOPK;
   m->ncand_fixed = m->fp32 ? 2 * ATT_TOPK : 2 * xatt_waves(m->d2) * XATT_TOPK;
-  m->ncand = m->ncand_fixed + (m->fp32 ? 0 : XATT_OVF);
+  m->ncand = m->ncand_fixed + (m->fp32 ? ATT_OVF : XATT_OVF);
   m->R = REFINE_R;
   m->att_tt = (m->fp32 || m->d2 <= 256) ? 128 : 64;
   m->splits = choose_splits(*m);
@@ -337,7 +337,7 @@ inline Plan make_plan(const still_config* c, const Dims& m) {
     }
     p.cval = take(4ul * m.splits * HCT * m.ncand);
     p.cidx = take(4ul * m.splits * HCT * m.ncand);
-    p.ocnt = m.fp32 ? 0 : take(4ul * m.splits * HCT);
+    p.ocnt = take(4ul * m.splits * HCT);
     p.ridx = take(4ul * HCT * m.R);
     p.rval = take(4ul * HCT * m.R);
     p.rcnt = take(4ul * HCT);

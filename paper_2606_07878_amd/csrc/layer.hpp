@@ -330,7 +330,7 @@ still_status run_layer(const still_config* cfg, const Dims& m, const Plan& p, ch
         a.keys_per_split = (int)m.keys_per_split;
         a.cval = (float*)(ws + p.cval);
         a.cidx = (int*)(ws + p.cidx);
-        a.ocnt = m.fp32 ? nullptr : (int*)(ws + p.ocnt);
+        a.ocnt = (int*)(ws + p.ocnt);
         a.xfeat = m.d2;
         a.xcoff = 0;
         hipError_t e;
