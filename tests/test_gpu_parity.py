@@ -43,6 +43,15 @@ def test_config1_positions_unsorted_fractional():
     _case(W1, positions=pos, name="cfg1 shuffled fractional positions")
 
 
+@pytest.mark.parametrize("mode", [configs.MODE_BF16, configs.MODE_FP32])
+def test_config1_large_positions(mode):
+    """Positions far into a long context (4.2 million, fractional steps): the
+    base-RoPE un-rotation, the compactor RoPE and the re-rotation take angles
+    of millions of radians, reduced in fp64."""
+    pos = 4194304.0 + np.arange(2048, dtype=np.float64) * 1.5
+    _case(W1, positions=pos, mode=mode, name=f"cfg1 positions from 4194304 mode{mode}")
+
+
 def test_config1_no_rerotate():
     _case(W1, rerotate=False, name="cfg1 no re-rotation")
 
