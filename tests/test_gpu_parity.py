@@ -32,7 +32,7 @@ def test_config1_full(mode):
     _case(W1, mode=mode, name=f"cfg1 mode{mode}")
 
 
-@pytest.mark.parametrize("N,t", [(1000, 100), (129, 7), (1, 1), (64, 1), (300, 300), (2048, 655)])
+@pytest.mark.parametrize("N,t", [(1000, 100), (129, 7), (1, 1), (64, 1), (300, 300), (2048, 655), (64, 200)])
 def test_config1_ragged_shapes(N, t):
     _case(W1, N=N, t=t, name=f"cfg1 N={N} t={t}")
 
