@@ -474,6 +474,41 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   const int pc = PAIRED ? P0 / (hh > 0 ? hh : 1) : 0;     // head of the wave's pairs (PAIR)
   const int pj0 = PAIRED ? P0 - pc * hh : 0;
   constexpr int RUN = BN / 4;
+  // PAIR: the bias values of the wave's pairs (the same for every slice),
+  // loaded before any store of the epilogue
+  float pbv0[PAIRED ? TN / 2 : 1], pbv1[PAIRED ? TN / 2 : 1];
+  if constexpr (EPI == EPI_PAIR) {
+#pragma unroll
+    for (int b = 0; b < TN / 2; ++b) {
+      const int x = b * 32 + l32;
+      const bool pv = P0 + x < N;
+      const int col0 = pc * g.hd + pj0 + x;
+      pbv0[b] = (bias && pv) ? to_f32(bias[col0]) : 0.f;
+      pbv1[b] = (bias && pv) ? to_f32(bias[col0 + hh]) : 0.f;
+    }
+  }
+  // PAIR: rotation table values of vector-pass step (slice a, step it),
+  // double-buffered so that each step's loads are issued before the previous
+  // step's stores (a load issued after a store waits for it)
+  constexpr int PV_ = 8, NIT_ = (EPI == EPI_PAIR) ? 32 * (RUN / PV_) / 64 : 1;
+  f32x4 tcs[2][PV_ / 2];
+  auto tab_load = [&](int a, int it, f32x4 (&dst)[PV_ / 2]) {
+    if constexpr (EPI == EPI_PAIR) {
+      constexpr int NV = RUN / PV_;
+      const int e = lane + 64 * it;
+      const int rl = e / NV, vx = (e % NV) * PV_;
+      int rgrp, rrow;
+      const bool rok = grow2(wm * (BM / 2) + a * 32 + rl, rgrp, rrow);
+      if (g.tab && rok && N - (P0 + vx) > 0) {
+        const long r = (long)rgrp * g.mgstride + rrow;
+        const int trow = (mg > 1 && g.mgstride == g.tab_mod) ? rrow : (int)r % g.tab_mod;
+        const float2* tp = g.tab + (long)trow * hh + pj0 + vx;
+#pragma unroll
+        for (int u = 0; u < PV_; u += 2) dst[u / 2] = *(const f32x4*)(tp + u);
+      }
+    }
+  };
+  if constexpr (EPI == EPI_PAIR) tab_load(0, 0, tcs[0]);
   // columns of run q, element x: global output column and validity
   auto run_col = [&](int q, int x) -> long {
     if constexpr (EPI == EPI_PAIR) return (long)pc * g.hd + pj0 + q * hh + x;
@@ -531,11 +566,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     } else {   // PAIR: biased pair members; rotation in the vector pass
 #pragma unroll
       for (int b = 0; b < TN / 2; ++b) {
-        const int x = b * 32 + l32;                 // position in the wave's run
-        const bool pv = P0 + x < N;
-        const int col0 = pc * g.hd + pj0 + x;
-        const float bv0 = (bias && pv) ? to_f32(bias[col0]) : 0.f;
-        const float bv1 = (bias && pv) ? to_f32(bias[col0 + hh]) : 0.f;
+        const float bv0 = pbv0[b], bv1 = pbv1[b];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const int rl = 8 * (j >> 2) + 4 * lg + (j & 3);
@@ -557,7 +588,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
       const int pidx = (pj0 / (BN / 2)) * 2 + wn;
 #pragma unroll
       for (int it = 0; it < 32 * NV / 64; ++it) {
+        static_assert(32 * NV / 64 == NIT_, "vector-pass steps");
         const int e = lane + 64 * it;
+        // the next step's table values (next slice's first step after the last)
+        if (it + 1 < NIT_) tab_load(a, it + 1, tcs[(a * NIT_ + it + 1) & 1]);
+        else if (a + 1 < TM) tab_load(a + 1, 0, tcs[(a * NIT_ + it + 1) & 1]);
         const int rl = e / NV, vx = (e % NV) * PV;
         int rgrp, rrow;
         const bool rok = grow2(lbase + rl, rgrp, rrow);
@@ -581,11 +616,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
           for (int u = 0; u < PV; ++u) sp += v0[u] * v0[u] + v1[u] * v1[u];
           const int jp = pj0 + vx;
           if (g.tab) {
-            const int trow = (mg > 1 && g.mgstride == g.tab_mod) ? rrow : (int)r % g.tab_mod;
-            const float2* tp = g.tab + (long)trow * hh + jp;
 #pragma unroll
             for (int u = 0; u < PV; u += 2) {
-              const f32x4 cs = *(const f32x4*)(tp + u);
+              const f32x4 cs = tcs[(a * NIT_ + it) & 1][u / 2];
               const float y00 = v0[u] * cs[0] - v1[u] * cs[1], y10 = v1[u] * cs[0] + v0[u] * cs[1];
               const float y01 = v0[u + 1] * cs[2] - v1[u + 1] * cs[3], y11 = v1[u + 1] * cs[2] + v0[u + 1] * cs[3];
               v0[u] = y00;
