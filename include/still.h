@@ -32,7 +32,15 @@
  *   evaluated as x W^T with the stored [out][in] array.
  * - Element type: STILL_MODE_BF16 -> every K, V, weight, bias, latent and
  *   output buffer holds bfloat16; STILL_MODE_FP32 -> float32 (validation
- *   mode, all internal arithmetic in fp32).  Positions are always float64.
+ *   mode: fp32 arithmetic, the near-maximal logits below in fp64).  Positions
+ *   are always float64.
+ * - Cross-attention logits (scaled by the head width, App. A) are computed
+ *   from fp16 (bf16 mode) or fp32 operands; every key whose logit lies within
+ *   10 log2 units of its latent's maximum is then recomputed accurately (fp32
+ *   from split fp16 operands, or fp64) and its weight replaced.  Capacity: 256
+ *   such keys per latent, from at most 1536 candidates per latent and key
+ *   split.  Caches with more near-maximal keys per latent (rows repeated
+ *   hundreds of times) exceed it and lose accuracy gradually.
  * - Work is enqueued on `stream` (NULL = default stream) and the call returns
  *   without synchronising.  Arguments are validated before anything is
  *   enqueued; a non-OK status means nothing was launched.  Faults during
