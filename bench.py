@@ -163,7 +163,7 @@ def summarize_counters(path: str, top: int = 400) -> None:
             parts.append(f"dram_write_MB={wr / 1e6:.1f} ({wr / us * 1e-6:.2f} TB/s)")
         for c in ("FETCH_SIZE", "WRITE_SIZE"):
             if c in m:
-                parts.append(f"{c}_KiB={m[c]:.6g}")
+                parts.append(f"{c}_KiB={m[c]:.1f}")
         print(f"{name} | " + " ".join(parts))
 
 
