@@ -77,6 +77,14 @@ def test_config1_variants(variant):
     _case(configs.shrink(W1, **ch), name=f"cfg1 {variant}")
 
 
+@pytest.mark.parametrize("H", [1, 4, 16])
+def test_kv_head_counts(H):
+    """KV head counts other than the benchmark's 8 and cfg 1's 2: the key
+    projection's workgroups then hold 128, 32 or 8 keys per KV head (its three
+    table-stage capacities), and every per-head grid dimension changes."""
+    _case(configs.shrink(W1, n_kv_heads=H), N=1000, t=200, name=f"cfg1 H={H}")
+
+
 @pytest.mark.parametrize("ds,t", [(128, 300), (128, 1024), (128, 1), (256, 257), (384, 300), (512, 100)])
 def test_self_attention_head_widths(ds, t):
     """Latent self-attention on the cfg-1 cache with self heads d_s wide: the
