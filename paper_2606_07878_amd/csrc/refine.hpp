@@ -8,7 +8,8 @@
 // rotated k~ with the query row q~_i.  The key row is carried at better than
 // fp16 precision as x_n = [K_hi | V | K_lo] (the RoPE-fixed key split into
 // two fp16 parts), contracted with [W_K | W_K(key half)]: one 3d-wide MFMA
-// product per slot.
+// product per slot, in which each W_K fragment of the key half serves both
+// the K_hi and the K_lo columns (2d columns of W_K streamed per row tile).
 //
 // Workgroup = BM candidate rows of one (h, c) list x all dc output widths.
 // The rows are gathered (base-RoPE un-rotation, hi/lo split) straight into
@@ -64,14 +65,14 @@ template <> __device__ __forceinline__ void load4f<bf16>(const bf16* p, float* o
 template <int D, int BM, class IT, class TBias>
 __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
   constexpr int W = 3 * D;               // contraction width [K_hi | V | K_lo]
-  constexpr int KS = W / 16;             // k steps
-  constexpr int KW = 2 * D / 16;         // k steps of W_K's 2d columns (K_lo wraps to step - KW)
+  constexpr int KW = 2 * D / 16;         // k steps of W_K's 2d columns
+  constexpr int KH = D / 16;             // key steps: K_hi and K_lo use the same W_K fragments
   constexpr int TC = BM / 32;            // candidate tiles (MFMA columns)
   constexpr int PT = 128;                // pairs per column tile (32 per wave)
   constexpr int LA = W + 8;              // LDS row stride (halfs)
-  constexpr int RB = 6;                  // W_K ring depth (k steps)
+  constexpr int RB = KW > 8 ? 8 : 4;     // W_K ring depth (k steps)
   constexpr int HD = D / 2;
-  static_assert(KS > RB && KS % RB == 0, "ring slots must repeat across column tiles");
+  static_assert(KW > RB && KW % RB == 0, "ring slots must repeat across column tiles");
   __shared__ __attribute__((aligned(16))) f16 As[BM * LA];
   __shared__ int2 rinfo[BM];             // (key, latent) of each row
   __shared__ float2 red[4][BM];
@@ -172,8 +173,7 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
     auto ct_ld = [&](int ct) { return (PT * ct + 32 * w < hh) ? PT * ct + 32 * w : 0; };
     auto load_b = [&](int pbase, int m, int s) -> half8 {
       const int row0 = pbase + m * hh;   // multiple of 32, row0 + 31 < dc
-      const int sk = s < KW ? s : s - KW;
-      return *(const half8*)(wkc + ((((long)(row0 >> 5) * KW + sk) << 9) + 8 * lane));
+      return *(const half8*)(wkc + ((((long)(row0 >> 5) * KW + s) << 9) + 8 * lane));
     };
 
     float dps[TC], sps[TC];
@@ -194,25 +194,36 @@ __global__ __launch_bounds__(256) void refine_kernel(RefineKArgs a) {
       f32x16 acc[TC][2];
 #pragma unroll
       for (int i = 0; i < TC; ++i) acc[i][0] = acc[i][1] = zero16();
-      half8 af[2][TC];
+      // step s < KH: [K_hi | K_lo] columns s of the rows against W_K's key
+      // step s (one W_K fragment, two products); s >= KH: the V columns
+      half8 af[2][TC], al[2][TC];
 #pragma unroll
-      for (int i = 0; i < TC; ++i) af[0][i] = *(const half8*)&Ab[32 * i * LA];
+      for (int i = 0; i < TC; ++i) {
+        af[0][i] = *(const half8*)&Ab[32 * i * LA];
+        al[0][i] = *(const half8*)&Ab[32 * i * LA + 2 * D];
+      }
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        if (s + 1 < KS) {
+      for (int s = 0; s < KW; ++s) {
+        if (s + 1 < KW) {
 #pragma unroll
-          for (int i = 0; i < TC; ++i) af[(s + 1) & 1][i] = *(const half8*)&Ab[32 * i * LA + 16 * (s + 1)];
+          for (int i = 0; i < TC; ++i) {
+            af[(s + 1) & 1][i] = *(const half8*)&Ab[32 * i * LA + 16 * (s + 1)];
+            if (s + 1 < KH) al[(s + 1) & 1][i] = *(const half8*)&Ab[32 * i * LA + 2 * D + 16 * (s + 1)];
+          }
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < TC; ++i)
 #pragma unroll
-          for (int m = 0; m < 2; ++m)
+          for (int m = 0; m < 2; ++m) {
             acc[i][m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(br[s % RB][m], af[s & 1][i], acc[i][m], 0, 0, 0);
+            if (s < KH)
+              acc[i][m] = __builtin_amdgcn_mfma_f32_32x32x16_f16(br[s % RB][m], al[s & 1][i], acc[i][m], 0, 0, 0);
+          }
         // refill the ring slot with step s + RB (of the next column tile past the end)
         const int sn = s + RB;
 #pragma unroll
-        for (int m = 0; m < 2; ++m) br[s % RB][m] = sn < KS ? load_b(ct_ld(ct), m, sn) : load_b(ctn, m, sn - KS);
+        for (int m = 0; m < 2; ++m) br[s % RB][m] = sn < KW ? load_b(ct_ld(ct), m, sn) : load_b(ctn, m, sn - KW);
         __builtin_amdgcn_sched_barrier(0);
       }
 
