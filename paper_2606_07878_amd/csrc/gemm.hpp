@@ -109,8 +109,8 @@ __device__ __forceinline__ void wave_lds_fence() {
 // LDS arena: two operand stages, reused after the k loop for the epilogue
 // staging (4 waves x 32 rows x (BN/2 + 8) floats).
 template <int BM, int BN, int BK, class CT>
-constexpr int gemm_lds_bytes() {
-  const int ops = 2 * (BM + BN) * BK * (int)sizeof(CT);
+constexpr int gemm_lds_bytes(int am = 1) {
+  const int ops = 2 * (am * BM + BN) * BK * (int)sizeof(CT);
   const int stg = 4 * 32 * (BN / 2 + 8) * 4;   // epilogue staging
   return ops > stg ? ops : stg;
 }
@@ -136,8 +136,12 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   constexpr int WC = TN * 32;
   constexpr int SLD = WC + 8;                  // staging row stride (floats): rows r and r+4 on disjoint banks
   static_assert(WC == BN / 2, "wave column count");
-  constexpr int LDSB = gemm_lds_bytes<BM, BN, BK, CT>();
-  constexpr int SS = (BM + BN) * LR;            // elements per stage: A rows, then B rows
+  // ST = 3: the direct-load path for a split A operand (C = (A + A2) B^T):
+  // each stage holds the k step of A, of A2 and of B, and each B fragment
+  // read from it serves both products (one pass over K instead of two)
+  constexpr int AM = ST == 3 ? 2 : 1;           // A operands per stage
+  constexpr int LDSB = gemm_lds_bytes<BM, BN, BK, CT>(AM);
+  constexpr int SS = (AM * BM + BN) * LR;       // elements per stage: A rows (A2 rows), then B rows
   static_assert(4 * 32 * SLD * 4 <= LDSB, "staging does not fit");
 
   __shared__ __attribute__((aligned(16))) unsigned char smem[LDSB];
@@ -382,28 +386,29 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
   // Rows past the end read row 0: they only reach outputs that are not stored.
   static_assert(sizeof(CT) == 2 && sizeof(TA) == 2 && sizeof(TB) == 2, "direct loads copy fp16 operands");
   constexpr int RPB = 512 / BK;                 // tile rows per 1 KB block
-  constexpr int NBLK = (BM + BN) / RPB;         // blocks per stage
+  constexpr int NBLK = (AM * BM + BN) / RPB;    // blocks per stage
   constexpr int NI = NBLK / 4;                  // blocks per wave and stage
-  static_assert(NBLK % 4 == 0 && BM % RPB == 0 && ST == 2, "direct load blocks");
+  static_assert(NBLK % 4 == 0 && BM % RPB == 0 && (ST == 2 || ST == 3), "direct load blocks");
   const int w = __builtin_amdgcn_readfirstlane(wave);
   // split A (C = (A + A2) B^T): a second pass over K reads the low part
   const CT* Alo = g.A2 ? (const CT*)g.A2 + b1 * g.sA1 + b2 * g.sA2 : nullptr;
   const int nk1 = K / BK;
-  const int nk = Alo ? 2 * nk1 : nk1;
+  const int nk = (Alo && AM == 1) ? 2 * nk1 : nk1;
   const CT* src[NI];     // first pass
   const CT* srclo[NI];   // second pass (A rows from A2; B rows unchanged)
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int rho = (i * 4 + w) * RPB + lane / KV;
-    const int u = (lane % KV) ^ lds_swz<KV>(rho);   // rho and rho - BM agree mod 16
-    if (rho < BM) {
-      const long gr = grow(rho);
+    const int u = (lane % KV) ^ lds_swz<KV>(rho);   // rho and rho - BM (rho - 2 BM) agree mod 16
+    if (rho < AM * BM) {
+      const bool second = rho >= BM;                 // AM = 2: rows of A2
+      const long gr = grow(second ? rho - BM : rho);
       const long off = (gr >= 0 ? gr * g.lda : 0) + u * E;
-      src[i] = (const CT*)A + off;
-      srclo[i] = Alo ? Alo + off : src[i];
+      src[i] = (second ? Alo : (const CT*)A) + off;
+      srclo[i] = (Alo && AM == 1) ? Alo + off : src[i];
     } else {
       bool valid;
-      const TB* bp = b_row(rho - BM, valid);
+      const TB* bp = b_row(rho - AM * BM, valid);
       src[i] = srclo[i] = (const CT*)(valid ? bp : B) + u * E;
     }
   }
@@ -425,12 +430,17 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
     __builtin_amdgcn_s_waitcnt((c & 15) | ((c >> 4) << 14) | 0x70);
   };
   auto compute = [&](const CT* Ac) {
-    const CT* Bc = Ac + BM * LR;
+    const CT* Bc = Ac + AM * BM * LR;
+    const CT* Lc = Ac + BM * LR;   // AM = 2: the A2 rows
     constexpr int KS = BK / (2 * E);
-    frag af[2][TM], bfr[2][TN];
+    frag af[2][TM], al[2][AM == 2 ? TM : 1], bfr[2][TN];
     auto rd = [&](int ks, int p) {
 #pragma unroll
       for (int a = 0; a < TM; ++a) af[p][a] = *(const frag*)&Ac[lds_at(wm * (BM / 2) + a * 32 + l32, ks * 2 + lg)];
+      if constexpr (AM == 2) {
+#pragma unroll
+        for (int a = 0; a < TM; ++a) al[p][a] = *(const frag*)&Lc[lds_at(wm * (BM / 2) + a * 32 + l32, ks * 2 + lg)];
+      }
 #pragma unroll
       for (int b = 0; b < TN; ++b) bfr[p][b] = *(const frag*)&Bc[lds_at(col_base(b) + l32, ks * 2 + lg)];
     };
@@ -442,7 +452,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int a = 0; a < TM; ++a)
 #pragma unroll
-        for (int b = 0; b < TN; ++b) MM::mma(acc[a][b], af[ks & 1][a], bfr[ks & 1][b]);
+        for (int b = 0; b < TN; ++b) {
+          MM::mma(acc[a][b], af[ks & 1][a], bfr[ks & 1][b]);
+          if constexpr (AM == 2) MM::mma(acc[a][b], al[ks & 1][a], bfr[ks & 1][b]);
+        }
       __builtin_amdgcn_sched_barrier(0);
     }
   };

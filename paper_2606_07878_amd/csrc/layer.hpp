@@ -37,8 +37,11 @@ static bool direct_ok(const GemmArgs& g, int bk, bool paired) {
 template <class CT, class TA, class TB, class TC, class TBias, int EPI, int BM, int BN, int BK>
 static hipError_t launch_pick(const GemmArgs& g, int batch, hipStream_t st) {
   if constexpr (std::is_same<CT, f16>::value && std::is_same<TA, f16>::value && std::is_same<TB, f16>::value) {
-    if (direct_ok(g, BK, EPI == EPI_PAIR || EPI == EPI_SWIGLU))
+    if (direct_ok(g, BK, EPI == EPI_PAIR || EPI == EPI_SWIGLU)) {
+      if constexpr (EPI == EPI_PAIR && BN == 256)
+        if (g.A2) return launch_gemm<CT, TA, TB, TC, TBias, EPI, BM, BN, BK, 3>(g, batch, st);
       return launch_gemm<CT, TA, TB, TC, TBias, EPI, BM, BN, BK, 2>(g, batch, st);
+    }
   }
   return launch_gemm<CT, TA, TB, TC, TBias, EPI, BM, BN, BK>(g, batch, st);
 }
